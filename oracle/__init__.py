@@ -1,0 +1,40 @@
+"""Float64 CPU oracle for paged-KV grouped-query attention.
+
+TEST INFRASTRUCTURE ONLY. Nothing on the product path may import, call or
+execute this package: only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` use it. It shares no code, constants or
+helpers with the HIP library; the only thing both sides share is the seeded
+input generator, which holds none of the attention arithmetic.
+
+What it computes (the plain definition, evaluated directly in float64):
+
+* decode  -- one query token per sequence attending to its whole cached
+  context (the batched generation of the rollout engines, paper section
+  "Fast Agentic Rollout with SGLang" and the rollout stage of the RL loop);
+* extend  -- a chunk of appended tokens attending to the cached prefix plus,
+  causally, to the chunk itself ("each turn prefills only the newly generated
+  suffix", same section, and the session server of section "Token-In-Token-Out");
+* merge   -- the log-sum-exp combination of attention results over disjoint
+  key ranges (split-KV partials).
+
+The paper names the attention kernels its engines run (section "True-On-Policy
+Alignment") but never writes the operation down; the definition used here is
+textbook scaled dot-product attention (Vaswani et al., 2017) with grouped-query
+head sharing (query head h reads KV head h // (Hq // Hkv)).
+
+Pins: see tests/test_oracle_pins.py (brute-force dense attention via scipy,
+single-key exactness, uniform-key closed form, page-size/page-order
+invariance, split/merge identity, extend<->decode and causal brute force,
+GQA expansion, scale homogeneity, batch permutation, closed-form golden file).
+Parity with values printed in the paper is unpinned: the paper prints none.
+"""
+
+from .attention import (  # noqa: F401
+    bf16_bits_to_f64,
+    gather_head,
+    attend,
+    attend_range,
+    decode,
+    extend,
+    merge,
+)
