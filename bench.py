@@ -1,0 +1,215 @@
+"""Benchmark of the rollout-attention hot path on one MI355X.
+
+One step = one pass of the whole path over resident synthetic batches:
+  * decode, agentic ragged batch (B=128, 96 query / 8 KV heads, lognormal
+    contexts, median 16K, clipped to [1K, 64K], page 64)  -> the headline;
+  * decode with trajectory-group prefix sharing (16 prompts x G=8, shared
+    4096-token prefix, private continuations U{512..16384});
+  * extend (B=32, cached prefix U{8K..64K}, appended chunk U{64..2048}).
+Prints one JSON line. ``value`` is the decode KV-bytes rate of the ragged 64K
+batch; the extend and prefix-group figures are reported beside it.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2516.6  # MI355X dense bf16 MFMA (256 CU x 4096 flop/clk x 2.4 GHz)
+METRIC = "decode-attention KV GB/s (% of HBM peak) + extend TFLOP/s at 64k ctx"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, tensors, budget_s: float):
+    """The float64 oracle on a bounded sample of the decode batch (host cores)."""
+    import numpy as np
+
+    import oracle
+    from paper_2609_08368_amd import workloads as wl
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # threadpoolctl missing: report the affinity set
+        threads = len(os.sched_getaffinity(0))
+    # smallest-first sample of sequences, grown until the estimated time budget is used
+    order = np.argsort(w.kv_lens, kind="stable")
+    done_tokens, elapsed, rows_done = 0, 0.0, 0
+    for b in order:
+        sub = wl.compact_subset(w, tensors, [int(b)])
+        t0 = time.perf_counter()
+        oracle.decode(sub["q"], sub["k_pages"], sub["v_pages"], sub["block_table"], sub["kv_lens"], tensors["scale"])
+        elapsed += time.perf_counter() - t0
+        done_tokens += int(w.kv_lens[b])
+        rows_done += 1
+        if elapsed >= budget_s:
+            break
+    kv_bytes = done_tokens * w.hkv * 128 * 2 * 2
+    return {"value": round(kv_bytes / elapsed / 1e9, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"float64 oracle decode of the {rows_done} shortest sequences of the ragged 64K batch "
+                      f"({done_tokens} keys, {kv_bytes / 1e9:.2f} GB of KV) in {elapsed:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (the kernels run on one device's share; "
+              "see DESIGN.md for how the work would shard). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_08368_amd import rl_attn as ra
+    from paper_2609_08368_amd import workloads as wl
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    ra.lib()
+    log("materialising inputs on the GPU ...")
+    w_dec = wl.decode_ragged()
+    w_grp = wl.decode_group_prefix()
+    w_ext = wl.extend_multiturn()
+    t_dec = wl.materialize(w_dec, dev, poison=False)
+    t_grp = wl.materialize(w_grp, dev, poison=False)
+    t_ext = wl.materialize(w_ext, dev, poison=False)
+    out_dec = torch.empty_like(t_dec["q"])
+    out_grp = torch.empty_like(t_grp["q"])
+    out_ext = torch.empty_like(t_ext["q"])
+    torch.cuda.synchronize()
+    log(f"ragged decode: sum(L)={int(w_dec.kv_lens.sum())}  group decode: sum(L)={int(w_grp.kv_lens.sum())}  "
+        f"extend: total_q={w_ext.total_q}")
+
+    def decode(w, t, out):
+        ra.decode_plain(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out)
+
+    def extend():
+        ra.extend_plain(t_ext["q"], t_ext["qo_indptr"], t_ext["k_pages"], t_ext["v_pages"], t_ext["block_table"],
+                        t_ext["kv_lens"], t_ext["scale"], out=out_ext)
+
+    parts = [("decode_ragged", lambda: decode(w_dec, t_dec, out_dec)),
+             ("decode_group_prefix", lambda: decode(w_grp, t_grp, out_grp)),
+             ("extend_multiturn", extend)]
+    for _ in range(args.warmup):
+        for _, fn in parts:
+            fn()
+    torch.cuda.synchronize()
+    log(f"warmup done; timing {args.steps} steps")
+
+    stream = torch.cuda.current_stream()
+    ev = {name: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                 for _ in range(args.steps)] for name, _ in parts}
+    ra.profile_read("decode")
+    ra.profile_read("extend")
+    ra.profile_enable(True)
+    torch.cuda.synchronize()
+    step_start = torch.cuda.Event(enable_timing=True)
+    step_stop = torch.cuda.Event(enable_timing=True)
+    step_start.record(stream)
+    for i in range(args.steps):
+        for name, fn in parts:
+            ev[name][i][0].record(stream)
+            fn()
+            ev[name][i][1].record(stream)
+    step_stop.record(stream)
+    torch.cuda.synchronize()
+    ra.profile_enable(False)
+    # kernel-level means: decode kernel launches alternate ragged / group (2 per step)
+    n_dec, dec_kernel_ms_all = ra.profile_read("decode")
+    n_ext, ext_kernel_ms = ra.profile_read("extend")
+    total_ms = step_start.elapsed_time(step_stop)
+    ms = {name: sorted(a.elapsed_time(b) for a, b in ev[name]) for name in ev}
+    med = {name: v[len(v) // 2] for name, v in ms.items()}
+    mean = {name: sum(v) / len(v) for name, v in ms.items()}
+
+    # separate kernel timing pass for the ragged decode alone (for the roofline)
+    ra.profile_enable(True)
+    for _ in range(args.steps):
+        parts[0][1]()
+    torch.cuda.synchronize()
+    ra.profile_enable(False)
+    n_k, dec_kernel_ms = ra.profile_read("decode")
+
+    kv_dec = w_dec.kv_bytes()
+    kv_grp_unique = w_grp.kv_bytes(unique=True)
+    kv_grp_logical = w_grp.kv_bytes()
+    kv_ext = w_ext.kv_bytes()
+    flops_ext = w_ext.flops()
+    dec_gbps = kv_dec / (mean["decode_ragged"] * 1e-3) / 1e9
+    kern_gbps = kv_dec / (dec_kernel_ms * 1e-3) / 1e9
+    ext_tflops = flops_ext / (mean["extend_multiturn"] * 1e-3) / 1e12
+    ext_kern_tflops = flops_ext / (ext_kernel_ms * 1e-3) / 1e12 if n_ext else None
+    grp_s = mean["decode_group_prefix"] * 1e-3
+
+    result = {
+        "metric": METRIC,
+        "value": round(dec_gbps, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(total_ms / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "step = decode of the agentic ragged batch (B128, Hq96/Hkv8, lognormal median 16K clipped "
+                        "1K-64K, page 64; value) + decode with trajectory-group prefix sharing (16x8, shared 4096, "
+                        "private 512-16384, Hq64/Hkv8) + extend (B32, prefix 8K-64K, chunk 64-2048, Hq64/Hkv8)",
+            "decode_batch": w_dec.batch, "decode_sum_kv_tokens": int(w_dec.kv_lens.sum()),
+            "decode_kv_bytes": kv_dec, "head_dim": 128, "page_size": 64, "seed": w_dec.seed,
+        },
+        "decode_ragged": {
+            "ms_mean": round(mean["decode_ragged"], 4), "ms_median": round(med["decode_ragged"], 4),
+            "kv_GBps": round(dec_gbps, 2), "hbm_frac": round(dec_gbps / HBM_PEAK_GBPS, 4),
+            "tokens_per_s": round(w_dec.batch / (mean["decode_ragged"] * 1e-3), 1),
+        },
+        "decode_group_prefix": {
+            "ms_mean": round(mean["decode_group_prefix"], 4),
+            "unique_kv_GBps": round(kv_grp_unique / grp_s / 1e9, 2),
+            "logical_kv_GBps": round(kv_grp_logical / grp_s / 1e9, 2),
+            "hbm_frac_unique": round(kv_grp_unique / grp_s / 1e9 / HBM_PEAK_GBPS, 4),
+            "tokens_per_s": round(w_grp.batch / grp_s, 1),
+        },
+        "extend_multiturn": {
+            "ms_mean": round(mean["extend_multiturn"], 4), "tflops": round(ext_tflops, 2),
+            "mfma_frac": round(ext_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+            "kernel_ms": round(ext_kernel_ms, 4) if n_ext else None,
+            "kernel_tflops": round(ext_kern_tflops, 2) if ext_kern_tflops else None,
+            "tokens_per_s": round(w_ext.total_q / (mean["extend_multiturn"] * 1e-3), 1),
+            "flops": flops_ext, "kv_bytes": kv_ext,
+        },
+        "roofline": {
+            "kernel": "decode_mfma_kernel (ragged 64K decode batch)",
+            "bound": "hbm", "achieved": round(kern_gbps, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(kern_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+            "kernel_ms": round(dec_kernel_ms, 4), "launches": n_k,
+            "algorithmic_bytes": kv_dec,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("timing the oracle on host cores ...")
+        result["cpu_baseline"] = cpu_baseline(w_dec, t_dec, args.cpu_budget)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,177 @@
+/*
+ * rl_attn.h -- paged-KV grouped-query attention for rollout engines (gfx950).
+ *
+ * The operation: the rollout engines of an RL post-training loop spend most
+ * of their time generating (paper, section "Rollout", opening paragraph), and
+ * each turn of an agentic session reuses the cached context of earlier turns,
+ * so a turn only prefills its newly appended suffix (section "Fast Agentic
+ * Rollout with SGLang"). That gives two attention calls over a paged KV cache:
+ *
+ *   decode : one query token per sequence attends to its whole context;
+ *   extend : a chunk of appended tokens attends to the cached prefix and,
+ *            causally, to itself.
+ *
+ * Trajectories of one group (G attempts at the same prompt, section "The
+ * Miles RL Loop") reference the same physical pages for the prompt, and the
+ * library reads such shared pages once per group.
+ *
+ * Math (scaled dot-product attention with grouped-query heads):
+ *   R = Hq / Hkv, query head h reads KV head g = h / R;
+ *   s_t = scale * dot(q[h], K[t, g]);  out[h] = sum_t softmax(s)_t V[t, g];
+ *   lse[h] = ln sum_t exp(s_t)  (natural log, scale included).
+ * Logical token t of sequence b lives in page block_table[b][t / P], slot t % P.
+ * Decode: t < seq_lens[b]. Extend: sequence b owns query rows
+ * qo_indptr[b] .. qo_indptr[b+1]-1 (n_b rows); its pages hold kv_lens[b]
+ * tokens, the last n_b of which are the chunk itself (already written);
+ * row i attends to t <= kv_lens[b] - n_b + i (bottom-right causal mask).
+ * An empty key range gives out = 0 and lse = -inf.
+ *
+ * Tensors: every argument is a non-owning view. dtype/ndim/shape are checked
+ * on the host; strides are in elements and free except that the last (head
+ * dimension) stride must be 1. All pointers are device pointers on the
+ * current HIP device. The library only reads q, pages, tables and lengths and
+ * only writes out / lse_out. Head dimension must be 128; Hq % Hkv == 0;
+ * page size P must be a power of two in [8, 128].
+ *
+ * Errors: every call returns RL_OK (0) or a negative RL_ERR_* code, and
+ * rl_attn_last_error() returns a thread-local message for the last failure on
+ * the calling thread. Host-side validation happens before any HIP call.
+ * Calls are asynchronous on `stream` (a hipStream_t; NULL = default stream);
+ * a launch failure returns RL_ERR_HIP. Calls on distinct streams are
+ * thread-safe. Page ids and lengths read on the device are clamped into the
+ * valid ranges, so no input can make a kernel read outside the given buffers;
+ * out-of-range values are counted in a device error word that
+ * rl_attn_check_device_errors() reports.
+ *
+ * Memory: the library owns one workspace per (device, stream), grown with
+ * hipMalloc on demand (or ahead of time with rl_attn_reserve_workspace) and
+ * never grown while the stream is being captured (RL_ERR_WORKSPACE instead).
+ */
+#ifndef RL_ATTN_H
+#define RL_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum rl_dtype { RL_BF16 = 1, RL_F32 = 2, RL_I32 = 3 };
+
+enum rl_status {
+  RL_OK = 0,
+  RL_ERR_INVALID_ARG = -1,  /* null pointer, negative size, bad option value   */
+  RL_ERR_SHAPE = -2,        /* shapes inconsistent with each other             */
+  RL_ERR_DTYPE = -3,        /* wrong element type                              */
+  RL_ERR_UNSUPPORTED = -4,  /* head_dim != 128, page size, non-unit last stride */
+  RL_ERR_WORKSPACE = -5,    /* workspace cannot be allocated (or capture)      */
+  RL_ERR_HIP = -6,          /* a HIP runtime call or kernel launch failed      */
+  RL_ERR_DEVICE = -7        /* device-side data errors were detected           */
+};
+
+/* Non-owning tensor view (DLPack-like). shape/strides beyond ndim are ignored. */
+typedef struct {
+  void* data;          /* device pointer (host pointers are never dereferenced) */
+  int32_t dtype;       /* enum rl_dtype                                         */
+  int32_t ndim;        /* 1..4                                                  */
+  int64_t shape[4];
+  int64_t strides[4];  /* in elements                                           */
+} rl_tensor;
+
+enum rl_prefix_mode { RL_PREFIX_AUTO = 0, RL_PREFIX_OFF = 1 };
+
+/* Options for the _ex calls. A NULL pointer means all defaults (zeros). */
+typedef struct {
+  int32_t split_tokens;  /* decode: tokens per split-KV partial; 0 = automatic,
+                            otherwise a multiple of 64 (RL_ERR_INVALID_ARG if not) */
+  int32_t prefix_share;  /* enum rl_prefix_mode: read group-shared prefix pages once
+                            (AUTO) or treat every sequence independently (OFF)     */
+  int32_t validate;      /* 1: also check every referenced page id on the device   */
+  int32_t reserved[5];   /* must be zero                                          */
+} rl_attn_opts;
+
+/* Batched decode (paper: batched generation by the rollout engines).
+ *   q           [B, Hq, 128] bf16
+ *   k_pages     [num_pages, P, Hkv, 128] bf16
+ *   v_pages     same shape and dtype as k_pages
+ *   block_table [B, max_pages] int32 (entries past ceil(seq_lens[b]/P) are never read)
+ *   seq_lens    [B] int32, 0 <= seq_lens[b] <= max_pages * P
+ *   scale       softmax scale (e.g. 1/sqrt(128))
+ *   out         [B, Hq, 128] bf16 (f32 also accepted), written
+ * Returns RL_OK or an RL_ERR_* code. */
+int rl_attn_decode(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages,
+                   const rl_tensor* block_table, const rl_tensor* seq_lens, float scale,
+                   rl_tensor* out, void* stream);
+
+/* Causal extend of appended chunks (paper: each turn prefills only its suffix).
+ *   q           [total_q, Hq, 128] bf16
+ *   qo_indptr   [B+1] int32, qo_indptr[0] = 0, non-decreasing, qo_indptr[B] = total_q
+ *   k_pages, v_pages, block_table as for decode
+ *   kv_lens     [B] int32, kv_lens[b] >= n_b (prefix + chunk)
+ *   out         [total_q, Hq, 128] bf16 (f32 also accepted), written */
+int rl_attn_extend(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor* k_pages,
+                   const rl_tensor* v_pages, const rl_tensor* block_table, const rl_tensor* kv_lens,
+                   float scale, rl_tensor* out, void* stream);
+
+/* Same as rl_attn_decode, plus an optional log-sum-exp output lse_out
+ * ([B, Hq] f32, natural log; NULL = not written) and options (NULL = defaults). */
+int rl_attn_decode_ex(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages,
+                      const rl_tensor* block_table, const rl_tensor* seq_lens, float scale,
+                      rl_tensor* out, rl_tensor* lse_out, const rl_attn_opts* opts, void* stream);
+
+/* Same as rl_attn_extend, plus lse_out ([total_q, Hq] f32, nullable) and options. */
+int rl_attn_extend_ex(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor* k_pages,
+                      const rl_tensor* v_pages, const rl_tensor* block_table, const rl_tensor* kv_lens,
+                      float scale, rl_tensor* out, rl_tensor* lse_out, const rl_attn_opts* opts,
+                      void* stream);
+
+/* Log-sum-exp merge of partial attention results over disjoint key ranges
+ * (the split-KV combine, exposed for testing and for callers that split work
+ * themselves):
+ *   o_parts   [N, S, H, 128] f32     lse_parts [N, S, H] f32 (natural log)
+ *   num_parts [N] int32, 0 <= num_parts[n] <= S (only the first num_parts[n] count)
+ *   out       [N, H, 128] bf16 or f32    lse_out [N, H] f32 (nullable)
+ * With M = max_s lse_s, w_s = exp(lse_s - M): out = sum w_s o_s / sum w_s,
+ * lse = M + ln sum w_s; parts with lse = -inf carry no weight; if all do,
+ * out = 0 and lse = -inf. */
+int rl_attn_merge(const rl_tensor* o_parts, const rl_tensor* lse_parts, const rl_tensor* num_parts,
+                  rl_tensor* out, rl_tensor* lse_out, void* stream);
+
+/* Thread-local message describing the last non-OK return on this thread. */
+const char* rl_attn_last_error(void);
+
+/* Synchronises `stream`, then returns RL_ERR_DEVICE if any call on this
+ * (device, stream) since the last check met an out-of-range page id, length
+ * or indptr on the device (those values were clamped), RL_OK otherwise, and
+ * clears the error word. */
+int rl_attn_check_device_errors(void* stream);
+
+/* Grows this (device, stream)'s workspace to at least `bytes` now, so later
+ * calls (e.g. under stream capture) need no allocation. */
+int rl_attn_reserve_workspace(size_t bytes, void* stream);
+
+/* Workspace bytes a decode / extend call with these sizes may need. */
+size_t rl_attn_decode_workspace_size(int64_t batch, int64_t num_q_heads, int64_t num_kv_heads,
+                                     int64_t max_pages, int64_t page_size);
+size_t rl_attn_extend_workspace_size(int64_t batch, int64_t total_q, int64_t num_q_heads,
+                                     int64_t num_kv_heads, int64_t max_pages, int64_t page_size);
+
+/* Kernel timing for benchmarks and profiling tools. While enabled, each
+ * decode / extend call brackets its main attention kernel with a pair of HIP
+ * events on the call's stream (the planner and combine kernels are outside
+ * the pair). rl_attn_profile_read() waits for the recorded events and returns
+ * the number of timed launches and their mean duration in milliseconds per
+ * kind (kind 0 = decode attention kernel, 1 = extend attention kernel), then
+ * forgets them. Disabled by default; enabling costs two event records per call. */
+int rl_attn_profile_enable(int on);
+int rl_attn_profile_read(int kind, int* launches, double* mean_ms);
+
+/* Frees every workspace the library holds (synchronises the device first). */
+void rl_attn_release(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RL_ATTN_H */

@@ -1,0 +1,112 @@
+// Kernel argument blocks and launchers (host-visible; no torch types anywhere).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rl {
+
+// Error bits accumulated in the device error word.
+enum DeviceError : int {
+  kErrLen = 1,       // a length outside [0, max_pages * P] (clamped)
+  kErrPage = 2,      // a page id outside [0, num_pages) (clamped)
+  kErrIndptr = 4,    // qo_indptr not non-decreasing within [0, total_q] (clamped)
+  kErrKvShort = 8,   // kv_lens[b] < chunk length (clamped up)
+};
+
+// Paged KV cache + block table, shared by decode and extend.
+struct PagedKV {
+  const void* k;          // [num_pages, P, Hkv, 128] bf16
+  const void* v;
+  int64_t sp, ss, sh;     // page / slot / head strides (elements), identical for K and V
+  int64_t v_sp, v_ss, v_sh;
+  const int* bt;          // [B, max_pages] int32
+  int64_t bt_sb, bt_sj;
+  int num_pages, page_size, log2_page, max_pages;
+};
+
+// Workspace carve-up of one decode or extend call.
+struct DecodePlanWs {
+  int* hdr;        // [0] split tokens, [1] number of work items
+  int* nsplit;     // [B]
+  int* base;       // [B] first work item of each sequence
+  int2* items;     // [max_items] (sequence, split index)
+  float* part_o;   // [max_items, Hq, 128]
+  float* part_lse; // [max_items, Hq]
+  int* err;        // device error word (persistent)
+};
+
+struct DecodeArgs {
+  PagedKV kv;
+  const void* q;
+  int64_t q_sb, q_sh;
+  const int* lens;
+  int64_t lens_s;
+  int B, Hq, Hkv, R;
+  float scale;
+  void* out;
+  int out_f32;
+  int64_t out_sb, out_sh;
+  float* lse;             // nullable
+  int64_t lse_sb, lse_sh;
+  int forced_split;       // 0 = choose on device
+  int target_items;       // work items the device planner aims for
+  int max_items;          // capacity of the item list / partial buffers
+  int prefix_share;       // 1 = read group-shared prefix pages once per group
+  int validate;
+  DecodePlanWs ws;
+};
+
+struct ExtendPlanWs {
+  int* hdr;        // [0] number of q tiles
+  int4* items;     // [max_items] (sequence, first chunk row, rows, key limit base)
+  int* err;
+};
+
+struct ExtendArgs {
+  PagedKV kv;
+  const void* q;
+  int64_t q_st, q_sh;
+  const int* qo_indptr;
+  const int* kv_lens;
+  int64_t kv_lens_s, indptr_s;
+  int B, total_q, Hq, Hkv, R;
+  int rows_head;          // query heads per tile (<= 64)
+  int tile_tokens;        // chunk tokens per tile
+  int head_blocks;        // ceil(R / rows_head)
+  float scale;
+  void* out;
+  int out_f32;
+  int64_t out_st, out_sh;
+  float* lse;
+  int64_t lse_st, lse_sh;
+  int max_items;
+  int validate;
+  ExtendPlanWs ws;
+};
+
+struct MergeArgs {
+  const float* o;        // [N, S, H, 128]
+  int64_t o_sn, o_ss, o_sh;
+  const float* lse;      // [N, S, H]
+  int64_t l_sn, l_ss, l_sh;
+  const int* num;        // [N]
+  int64_t num_s;
+  int N, S, H;
+  void* out;
+  int out_f32;
+  int64_t out_sn, out_sh;
+  float* lse_out;
+  int64_t lo_sn, lo_sh;
+};
+
+// Optional events around the main attention kernel (benchmark timing).
+struct KernelTimer {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream, KernelTimer* timer);
+hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream, KernelTimer* timer);
+hipError_t launch_merge(const MergeArgs& a, hipStream_t stream);
+
+}  // namespace rl

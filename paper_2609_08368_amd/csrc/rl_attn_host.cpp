@@ -1,0 +1,681 @@
+// Host side of the C-ABI: argument validation, per-(device, stream)
+// workspaces, error reporting and kernel dispatch. Every check that can fail
+// on the host runs before the first HIP runtime call.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "kernels.hpp"
+#include "rl_attn.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(RL_ERR_HIP, "%s failed: %s", what, hipGetErrorString(e));
+}
+
+// ------------------------------------------------------------------ options
+struct EnvDefaults {
+  int split_tokens = 0;
+  int prefix_share = RL_PREFIX_AUTO;
+  int validate = 0;
+  int target_wgs_per_cu = 64;
+  bool fail_alloc = false;
+};
+
+const EnvDefaults& env() {
+  static EnvDefaults d = [] {
+    EnvDefaults e;
+    if (const char* s = std::getenv("RL_ATTN_SPLIT_TOKENS")) e.split_tokens = std::atoi(s);
+    if (const char* s = std::getenv("RL_ATTN_PREFIX_SHARE")) e.prefix_share = std::strcmp(s, "off") == 0;
+    if (const char* s = std::getenv("RL_ATTN_VALIDATE")) e.validate = std::atoi(s) != 0;
+    if (const char* s = std::getenv("RL_ATTN_TARGET_WGS_PER_CU")) e.target_wgs_per_cu = std::max(1, std::atoi(s));
+    if (const char* s = std::getenv("RL_ATTN_TEST_FAIL_ALLOC")) e.fail_alloc = std::atoi(s) != 0;
+    return e;
+  }();
+  return d;
+}
+
+struct Opts {
+  int split_tokens, prefix_share, validate;
+};
+
+int read_opts(const rl_attn_opts* o, Opts* out) {
+  const EnvDefaults& e = env();
+  *out = {e.split_tokens, e.prefix_share, e.validate};
+  if (!o) return RL_OK;
+  for (int i = 0; i < 5; ++i)
+    if (o->reserved[i] != 0) return fail(RL_ERR_INVALID_ARG, "opts.reserved[%d] must be zero", i);
+  if (o->split_tokens < 0 || o->split_tokens % 64 != 0)
+    return fail(RL_ERR_INVALID_ARG, "opts.split_tokens must be 0 or a positive multiple of 64 (got %d)",
+                o->split_tokens);
+  if (o->prefix_share != RL_PREFIX_AUTO && o->prefix_share != RL_PREFIX_OFF)
+    return fail(RL_ERR_INVALID_ARG, "opts.prefix_share must be RL_PREFIX_AUTO or RL_PREFIX_OFF");
+  if (o->validate != 0 && o->validate != 1) return fail(RL_ERR_INVALID_ARG, "opts.validate must be 0 or 1");
+  if (o->split_tokens) out->split_tokens = o->split_tokens;
+  out->prefix_share = o->prefix_share;
+  out->validate = o->validate || e.validate;
+  return RL_OK;
+}
+
+// --------------------------------------------------------------- validation
+const char* dtype_name(int d) {
+  switch (d) {
+    case RL_BF16: return "bf16";
+    case RL_F32: return "f32";
+    case RL_I32: return "int32";
+    default: return "unknown";
+  }
+}
+
+int check_view(const rl_tensor* t, const char* name, int ndim) {
+  if (!t) return fail(RL_ERR_INVALID_ARG, "%s is NULL", name);
+  if (t->ndim != ndim) return fail(RL_ERR_SHAPE, "%s must have %d dimensions (got %d)", name, ndim, t->ndim);
+  for (int i = 0; i < ndim; ++i)
+    if (t->shape[i] < 0) return fail(RL_ERR_INVALID_ARG, "%s.shape[%d] is negative", name, i);
+  return RL_OK;
+}
+
+int64_t numel(const rl_tensor* t) {
+  int64_t n = 1;
+  for (int i = 0; i < t->ndim; ++i) n *= t->shape[i];
+  return n;
+}
+
+int check_data(const rl_tensor* t, const char* name) {
+  if (numel(t) > 0 && !t->data) return fail(RL_ERR_INVALID_ARG, "%s.data is NULL", name);
+  return RL_OK;
+}
+
+int check_dtype(const rl_tensor* t, const char* name, int dtype) {
+  if (t->dtype != dtype)
+    return fail(RL_ERR_DTYPE, "%s must be %s (got %s)", name, dtype_name(dtype), dtype_name(t->dtype));
+  return RL_OK;
+}
+
+// A tensor whose last dimension is the 128-wide head dimension, read or
+// written 16 bytes at a time: unit last stride, other strides multiples of
+// 8 elements, 16-byte aligned base.
+int check_rows128(const rl_tensor* t, const char* name) {
+  if (t->shape[t->ndim - 1] != 128)
+    return fail(RL_ERR_UNSUPPORTED, "%s: head dimension must be 128 (got %lld)", name,
+                (long long)t->shape[t->ndim - 1]);
+  if (t->strides[t->ndim - 1] != 1) return fail(RL_ERR_UNSUPPORTED, "%s: last stride must be 1", name);
+  for (int i = 0; i < t->ndim - 1; ++i)
+    if (t->strides[i] % 8 != 0 || t->strides[i] < 0)
+      return fail(RL_ERR_UNSUPPORTED, "%s: stride[%d] must be a non-negative multiple of 8 elements", name, i);
+  if (reinterpret_cast<uintptr_t>(t->data) % 16 != 0)
+    return fail(RL_ERR_UNSUPPORTED, "%s: data must be 16-byte aligned", name);
+  return RL_OK;
+}
+
+#define RL_TRY(x)          \
+  do {                     \
+    int rc_ = (x);         \
+    if (rc_ != RL_OK) return rc_; \
+  } while (0)
+
+// ---------------------------------------------------------------- workspace
+struct Workspace {
+  void* ptr = nullptr;
+  size_t size = 0;
+  int* err = nullptr;
+};
+
+std::mutex g_mu;
+std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+std::map<int, int> g_cus;
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int device_cus(int dev) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  auto it = g_cus.find(dev);
+  if (it != g_cus.end()) return it->second;
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+  g_cus[dev] = n;
+  return n;
+}
+
+int acquire_ws(hipStream_t st, size_t need, Workspace** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lk(g_mu);
+  Workspace& w = g_ws[{dev, st}];
+  const bool need_err = w.err == nullptr;
+  const bool grow = w.size < need;
+  if (need_err || grow) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone)
+      return fail(RL_ERR_WORKSPACE,
+                  "workspace must grow to %zu bytes while the stream is being captured; call "
+                  "rl_attn_reserve_workspace first",
+                  need);
+    if (env().fail_alloc) return fail(RL_ERR_WORKSPACE, "workspace allocation failed (RL_ATTN_TEST_FAIL_ALLOC)");
+  }
+  if (need_err) {
+    void* p = nullptr;
+    e = hipMalloc(&p, 256);
+    if (e != hipSuccess) return fail(RL_ERR_WORKSPACE, "hipMalloc(256) for the error word failed: %s", hipGetErrorString(e));
+    e = hipMemset(p, 0, 256);
+    if (e != hipSuccess) return hip_fail(e, "hipMemset");
+    w.err = static_cast<int*>(p);
+  }
+  if (grow) {
+    if (w.ptr) {
+      e = hipStreamSynchronize(st);
+      if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+      (void)hipFree(w.ptr);
+      w.ptr = nullptr;
+      w.size = 0;
+    }
+    void* p = nullptr;
+    e = hipMalloc(&p, need);
+    if (e != hipSuccess) return fail(RL_ERR_WORKSPACE, "hipMalloc(%zu) for the workspace failed: %s", need, hipGetErrorString(e));
+    w.ptr = p;
+    w.size = need;
+  }
+  *out = &w;
+  return RL_OK;
+}
+
+// ------------------------------------------------------------ kernel timing
+struct Profiler {
+  std::mutex mu;
+  bool on = false;
+  std::vector<rl::KernelTimer> pending[2];
+};
+
+Profiler& prof() {
+  static Profiler p;
+  return p;
+}
+
+// Returns a timer to pass to a launch when profiling is on (else nullptr).
+rl::KernelTimer* prof_timer(rl::KernelTimer* slot) {
+  Profiler& p = prof();
+  std::lock_guard<std::mutex> lk(p.mu);
+  if (!p.on) return nullptr;
+  if (hipEventCreate(&slot->start) != hipSuccess) return nullptr;
+  if (hipEventCreate(&slot->stop) != hipSuccess) {
+    (void)hipEventDestroy(slot->start);
+    return nullptr;
+  }
+  return slot;
+}
+
+void prof_commit(int kind, rl::KernelTimer* t) {
+  if (!t) return;
+  Profiler& p = prof();
+  std::lock_guard<std::mutex> lk(p.mu);
+  p.pending[kind].push_back(*t);
+}
+
+// ------------------------------------------------------------------- decode
+struct DecodeLayout {
+  int max_items;
+  size_t off_nsplit, off_base, off_items, off_po, off_pl, total;
+};
+
+DecodeLayout decode_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t max_pages, int64_t P, int split, int cus) {
+  DecodeLayout L{};
+  const int64_t R = Hq / std::max<int64_t>(1, Hkv);
+  const int64_t per_item = Hkv * (R == 1 ? 1 : (R + 15) / 16);
+  const int64_t max_tokens = max_pages * P;
+  int64_t items;
+  if (split > 0)
+    items = B * std::max<int64_t>(1, (max_tokens + split - 1) / split);
+  else
+    items = B + std::max<int64_t>(1, (int64_t)cus * env().target_wgs_per_cu / std::max<int64_t>(1, per_item));
+  L.max_items = (int)std::min<int64_t>(items, INT32_MAX / 2);
+  size_t off = 256;  // header
+  L.off_nsplit = off;
+  off += align256(B * 4);
+  L.off_base = off;
+  off += align256(B * 4);
+  L.off_items = off;
+  off += align256((size_t)L.max_items * 8);
+  L.off_po = off;
+  off += align256((size_t)L.max_items * Hq * 128 * 4);
+  L.off_pl = off;
+  off += align256((size_t)L.max_items * Hq * 4);
+  L.total = off;
+  return L;
+}
+
+int target_items_for(int64_t Hq, int64_t Hkv, int cus) {
+  const int64_t R = Hq / Hkv;
+  const int64_t per_item = Hkv * (R == 1 ? 1 : (R + 15) / 16);
+  return (int)std::max<int64_t>(1, (int64_t)cus * env().target_wgs_per_cu / per_item);
+}
+
+int fill_paged(const rl_tensor* k, const rl_tensor* v, const rl_tensor* bt, int64_t B, rl::PagedKV* kv) {
+  RL_TRY(check_view(k, "k_pages", 4));
+  RL_TRY(check_view(v, "v_pages", 4));
+  RL_TRY(check_view(bt, "block_table", 2));
+  RL_TRY(check_dtype(k, "k_pages", RL_BF16));
+  RL_TRY(check_dtype(v, "v_pages", RL_BF16));
+  RL_TRY(check_dtype(bt, "block_table", RL_I32));
+  for (int i = 0; i < 4; ++i)
+    if (k->shape[i] != v->shape[i]) return fail(RL_ERR_SHAPE, "k_pages and v_pages shapes differ (dim %d)", i);
+  RL_TRY(check_rows128(k, "k_pages"));
+  RL_TRY(check_rows128(v, "v_pages"));
+  const int64_t P = k->shape[1];
+  if (P < 8 || P > 128 || (P & (P - 1)) != 0)
+    return fail(RL_ERR_UNSUPPORTED, "page size must be a power of two in [8, 128] (got %lld)", (long long)P);
+  if (bt->shape[0] != B)
+    return fail(RL_ERR_SHAPE, "block_table.shape[0] (%lld) != batch (%lld)", (long long)bt->shape[0], (long long)B);
+  if (k->shape[0] < 1 && bt->shape[1] > 0) return fail(RL_ERR_SHAPE, "the page pool is empty");
+  if (k->shape[0] > INT32_MAX || bt->shape[1] * P > INT32_MAX)
+    return fail(RL_ERR_UNSUPPORTED, "page pool or block table too large for 32-bit token indices");
+  RL_TRY(check_data(k, "k_pages"));
+  RL_TRY(check_data(v, "v_pages"));
+  RL_TRY(check_data(bt, "block_table"));
+  kv->k = k->data;
+  kv->v = v->data;
+  kv->sp = k->strides[0];
+  kv->ss = k->strides[1];
+  kv->sh = k->strides[2];
+  kv->v_sp = v->strides[0];
+  kv->v_ss = v->strides[1];
+  kv->v_sh = v->strides[2];
+  kv->bt = static_cast<const int*>(bt->data);
+  kv->bt_sb = bt->strides[0];
+  kv->bt_sj = bt->strides[1];
+  kv->num_pages = (int)k->shape[0];
+  kv->page_size = (int)P;
+  int lg = 0;
+  while ((1 << lg) < P) ++lg;
+  kv->log2_page = lg;
+  kv->max_pages = (int)bt->shape[1];
+  return RL_OK;
+}
+
+int check_out(const rl_tensor* out, const rl_tensor* q, const char* name, int* is_f32) {
+  RL_TRY(check_view(out, name, 3));
+  if (out->dtype != RL_BF16 && out->dtype != RL_F32)
+    return fail(RL_ERR_DTYPE, "%s must be bf16 or f32 (got %s)", name, dtype_name(out->dtype));
+  for (int i = 0; i < 3; ++i)
+    if (out->shape[i] != q->shape[i]) return fail(RL_ERR_SHAPE, "%s shape must equal q's (dim %d)", name, i);
+  RL_TRY(check_rows128(out, name));
+  RL_TRY(check_data(out, name));
+  *is_f32 = out->dtype == RL_F32;
+  return RL_OK;
+}
+
+int check_lse(const rl_tensor* lse, int64_t rows, int64_t heads) {
+  if (!lse) return RL_OK;
+  RL_TRY(check_view(lse, "lse_out", 2));
+  RL_TRY(check_dtype(lse, "lse_out", RL_F32));
+  if (lse->shape[0] != rows || lse->shape[1] != heads) return fail(RL_ERR_SHAPE, "lse_out shape mismatch");
+  RL_TRY(check_data(lse, "lse_out"));
+  return RL_OK;
+}
+
+int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages, const rl_tensor* block_table,
+                const rl_tensor* seq_lens, float scale, rl_tensor* out, rl_tensor* lse_out, const rl_attn_opts* opts,
+                void* stream) {
+  Opts o;
+  RL_TRY(read_opts(opts, &o));
+  RL_TRY(check_view(q, "q", 3));
+  RL_TRY(check_dtype(q, "q", RL_BF16));
+  RL_TRY(check_rows128(q, "q"));
+  const int64_t B = q->shape[0], Hq = q->shape[1];
+  rl::DecodeArgs a{};
+  RL_TRY(fill_paged(k_pages, v_pages, block_table, B, &a.kv));
+  const int64_t Hkv = k_pages->shape[2];
+  if (Hkv < 1 || Hq < 1 || Hq % Hkv != 0)
+    return fail(RL_ERR_SHAPE, "query heads (%lld) must be a positive multiple of KV heads (%lld)", (long long)Hq,
+                (long long)Hkv);
+  RL_TRY(check_view(seq_lens, "seq_lens", 1));
+  RL_TRY(check_dtype(seq_lens, "seq_lens", RL_I32));
+  if (seq_lens->shape[0] != B) return fail(RL_ERR_SHAPE, "seq_lens.shape[0] != batch");
+  int is_f32 = 0;
+  RL_TRY(check_out(out, q, "out", &is_f32));
+  RL_TRY(check_lse(lse_out, B, Hq));
+  if (B > (1 << 22) || Hq > 4096) return fail(RL_ERR_UNSUPPORTED, "batch or head count too large");
+  RL_TRY(check_data(q, "q"));
+  RL_TRY(check_data(seq_lens, "seq_lens"));
+  if (B == 0) return RL_OK;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  const int cus = device_cus(dev);
+  const DecodeLayout lay = decode_layout(B, Hq, Hkv, a.kv.max_pages, a.kv.page_size, o.split_tokens, cus);
+  Workspace* w = nullptr;
+  RL_TRY(acquire_ws(st, lay.total, &w));
+  char* base = static_cast<char*>(w->ptr);
+  a.q = q->data;
+  a.q_sb = q->strides[0];
+  a.q_sh = q->strides[1];
+  a.lens = static_cast<const int*>(seq_lens->data);
+  a.lens_s = seq_lens->strides[0];
+  a.B = (int)B;
+  a.Hq = (int)Hq;
+  a.Hkv = (int)Hkv;
+  a.R = (int)(Hq / Hkv);
+  a.scale = scale;
+  a.out = out->data;
+  a.out_f32 = is_f32;
+  a.out_sb = out->strides[0];
+  a.out_sh = out->strides[1];
+  a.lse = lse_out ? static_cast<float*>(lse_out->data) : nullptr;
+  a.lse_sb = lse_out ? lse_out->strides[0] : 0;
+  a.lse_sh = lse_out ? lse_out->strides[1] : 0;
+  a.forced_split = o.split_tokens;
+  a.target_items = target_items_for(Hq, Hkv, cus);
+  a.max_items = lay.max_items;
+  a.prefix_share = o.prefix_share == RL_PREFIX_AUTO;
+  a.validate = o.validate;
+  a.ws.hdr = reinterpret_cast<int*>(base);
+  a.ws.nsplit = reinterpret_cast<int*>(base + lay.off_nsplit);
+  a.ws.base = reinterpret_cast<int*>(base + lay.off_base);
+  a.ws.items = reinterpret_cast<int2*>(base + lay.off_items);
+  a.ws.part_o = reinterpret_cast<float*>(base + lay.off_po);
+  a.ws.part_lse = reinterpret_cast<float*>(base + lay.off_pl);
+  a.ws.err = w->err;
+  rl::KernelTimer slot;
+  rl::KernelTimer* timer = prof_timer(&slot);
+  e = rl::launch_decode(a, st, timer);
+  prof_commit(0, timer);
+  if (e != hipSuccess) return hip_fail(e, "decode kernel launch");
+  return RL_OK;
+}
+
+// ------------------------------------------------------------------- extend
+struct ExtendShape {
+  int rows_head, tile_tokens, head_blocks;
+};
+
+ExtendShape extend_shape(int64_t R) {
+  ExtendShape s;
+  s.rows_head = (int)std::min<int64_t>(R, 128);
+  s.tile_tokens = std::max(1, 128 / s.rows_head);
+  s.head_blocks = (int)((R + s.rows_head - 1) / s.rows_head);
+  return s;
+}
+
+size_t extend_ws_bytes(int64_t B, int64_t total_q, int64_t R, int* max_items) {
+  const ExtendShape s = extend_shape(R);
+  const int64_t items = B + (total_q + s.tile_tokens - 1) / s.tile_tokens;
+  *max_items = (int)std::min<int64_t>(items, INT32_MAX / 2);
+  return 256 + align256((size_t)*max_items * 16);
+}
+
+int extend_impl(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor* k_pages, const rl_tensor* v_pages,
+                const rl_tensor* block_table, const rl_tensor* kv_lens, float scale, rl_tensor* out,
+                rl_tensor* lse_out, const rl_attn_opts* opts, void* stream) {
+  Opts o;
+  RL_TRY(read_opts(opts, &o));
+  RL_TRY(check_view(q, "q", 3));
+  RL_TRY(check_dtype(q, "q", RL_BF16));
+  RL_TRY(check_rows128(q, "q"));
+  RL_TRY(check_view(kv_lens, "kv_lens", 1));
+  RL_TRY(check_dtype(kv_lens, "kv_lens", RL_I32));
+  RL_TRY(check_view(qo_indptr, "qo_indptr", 1));
+  RL_TRY(check_dtype(qo_indptr, "qo_indptr", RL_I32));
+  const int64_t B = kv_lens->shape[0];
+  if (qo_indptr->shape[0] != B + 1)
+    return fail(RL_ERR_SHAPE, "qo_indptr must have batch + 1 = %lld entries (got %lld)", (long long)(B + 1),
+                (long long)qo_indptr->shape[0]);
+  const int64_t total_q = q->shape[0], Hq = q->shape[1];
+  rl::ExtendArgs a{};
+  RL_TRY(fill_paged(k_pages, v_pages, block_table, B, &a.kv));
+  const int64_t Hkv = k_pages->shape[2];
+  if (Hkv < 1 || Hq < 1 || Hq % Hkv != 0)
+    return fail(RL_ERR_SHAPE, "query heads (%lld) must be a positive multiple of KV heads (%lld)", (long long)Hq,
+                (long long)Hkv);
+  int is_f32 = 0;
+  RL_TRY(check_out(out, q, "out", &is_f32));
+  RL_TRY(check_lse(lse_out, total_q, Hq));
+  if (B > (1 << 22) || total_q > INT32_MAX / 2 || Hq > 4096)
+    return fail(RL_ERR_UNSUPPORTED, "batch, query rows or head count too large");
+  RL_TRY(check_data(q, "q"));
+  RL_TRY(check_data(kv_lens, "kv_lens"));
+  RL_TRY(check_data(qo_indptr, "qo_indptr"));
+  if (B == 0 || total_q == 0) return RL_OK;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int max_items = 0;
+  const size_t bytes = extend_ws_bytes(B, total_q, Hq / Hkv, &max_items);
+  Workspace* w = nullptr;
+  RL_TRY(acquire_ws(st, bytes, &w));
+  char* base = static_cast<char*>(w->ptr);
+  const ExtendShape s = extend_shape(Hq / Hkv);
+  a.q = q->data;
+  a.q_st = q->strides[0];
+  a.q_sh = q->strides[1];
+  a.qo_indptr = static_cast<const int*>(qo_indptr->data);
+  a.indptr_s = qo_indptr->strides[0];
+  a.kv_lens = static_cast<const int*>(kv_lens->data);
+  a.kv_lens_s = kv_lens->strides[0];
+  a.B = (int)B;
+  a.total_q = (int)total_q;
+  a.Hq = (int)Hq;
+  a.Hkv = (int)Hkv;
+  a.R = (int)(Hq / Hkv);
+  a.rows_head = s.rows_head;
+  a.tile_tokens = s.tile_tokens;
+  a.head_blocks = s.head_blocks;
+  a.scale = scale;
+  a.out = out->data;
+  a.out_f32 = is_f32;
+  a.out_st = out->strides[0];
+  a.out_sh = out->strides[1];
+  a.lse = lse_out ? static_cast<float*>(lse_out->data) : nullptr;
+  a.lse_st = lse_out ? lse_out->strides[0] : 0;
+  a.lse_sh = lse_out ? lse_out->strides[1] : 0;
+  a.max_items = max_items;
+  a.validate = o.validate;
+  a.ws.hdr = reinterpret_cast<int*>(base);
+  a.ws.items = reinterpret_cast<int4*>(base + 256);
+  a.ws.err = w->err;
+  rl::KernelTimer slot;
+  rl::KernelTimer* timer = prof_timer(&slot);
+  hipError_t e = rl::launch_extend(a, st, timer);
+  prof_commit(1, timer);
+  if (e != hipSuccess) return hip_fail(e, "extend kernel launch");
+  return RL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int rl_attn_decode(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages,
+                   const rl_tensor* block_table, const rl_tensor* seq_lens, float scale, rl_tensor* out,
+                   void* stream) {
+  return decode_impl(q, k_pages, v_pages, block_table, seq_lens, scale, out, nullptr, nullptr, stream);
+}
+
+int rl_attn_decode_ex(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages,
+                      const rl_tensor* block_table, const rl_tensor* seq_lens, float scale, rl_tensor* out,
+                      rl_tensor* lse_out, const rl_attn_opts* opts, void* stream) {
+  return decode_impl(q, k_pages, v_pages, block_table, seq_lens, scale, out, lse_out, opts, stream);
+}
+
+int rl_attn_extend(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor* k_pages,
+                   const rl_tensor* v_pages, const rl_tensor* block_table, const rl_tensor* kv_lens, float scale,
+                   rl_tensor* out, void* stream) {
+  return extend_impl(q, qo_indptr, k_pages, v_pages, block_table, kv_lens, scale, out, nullptr, nullptr, stream);
+}
+
+int rl_attn_extend_ex(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor* k_pages,
+                      const rl_tensor* v_pages, const rl_tensor* block_table, const rl_tensor* kv_lens, float scale,
+                      rl_tensor* out, rl_tensor* lse_out, const rl_attn_opts* opts, void* stream) {
+  return extend_impl(q, qo_indptr, k_pages, v_pages, block_table, kv_lens, scale, out, lse_out, opts, stream);
+}
+
+int rl_attn_merge(const rl_tensor* o_parts, const rl_tensor* lse_parts, const rl_tensor* num_parts, rl_tensor* out,
+                  rl_tensor* lse_out, void* stream) {
+  RL_TRY(check_view(o_parts, "o_parts", 4));
+  RL_TRY(check_dtype(o_parts, "o_parts", RL_F32));
+  RL_TRY(check_view(lse_parts, "lse_parts", 3));
+  RL_TRY(check_dtype(lse_parts, "lse_parts", RL_F32));
+  RL_TRY(check_view(num_parts, "num_parts", 1));
+  RL_TRY(check_dtype(num_parts, "num_parts", RL_I32));
+  RL_TRY(check_view(out, "out", 3));
+  if (out->dtype != RL_BF16 && out->dtype != RL_F32) return fail(RL_ERR_DTYPE, "out must be bf16 or f32");
+  if (o_parts->shape[3] != 128 || out->shape[2] != 128)
+    return fail(RL_ERR_UNSUPPORTED, "head dimension must be 128");
+  if (o_parts->strides[3] != 1 || out->strides[2] != 1) return fail(RL_ERR_UNSUPPORTED, "last stride must be 1");
+  const int64_t N = o_parts->shape[0], S = o_parts->shape[1], H = o_parts->shape[2];
+  if (lse_parts->shape[0] != N || lse_parts->shape[1] != S || lse_parts->shape[2] != H)
+    return fail(RL_ERR_SHAPE, "lse_parts shape must be [N, S, H] of o_parts");
+  if (num_parts->shape[0] != N) return fail(RL_ERR_SHAPE, "num_parts must have N entries");
+  if (out->shape[0] != N || out->shape[1] != H) return fail(RL_ERR_SHAPE, "out shape must be [N, H, 128]");
+  RL_TRY(check_lse(lse_out, N, H));
+  for (int i = 0; i < 3; ++i)
+    if (o_parts->strides[i] % 2 != 0) return fail(RL_ERR_UNSUPPORTED, "o_parts strides must be even");
+  if (reinterpret_cast<uintptr_t>(o_parts->data) % 8 != 0) return fail(RL_ERR_UNSUPPORTED, "o_parts must be 8-byte aligned");
+  if (N > INT32_MAX / 4096 || H > 4096 || S > INT32_MAX) return fail(RL_ERR_UNSUPPORTED, "merge sizes too large");
+  RL_TRY(check_data(o_parts, "o_parts"));
+  RL_TRY(check_data(lse_parts, "lse_parts"));
+  RL_TRY(check_data(num_parts, "num_parts"));
+  RL_TRY(check_data(out, "out"));
+  if (N == 0 || H == 0) return RL_OK;
+  rl::MergeArgs a{};
+  a.o = static_cast<const float*>(o_parts->data);
+  a.o_sn = o_parts->strides[0];
+  a.o_ss = o_parts->strides[1];
+  a.o_sh = o_parts->strides[2];
+  a.lse = static_cast<const float*>(lse_parts->data);
+  a.l_sn = lse_parts->strides[0];
+  a.l_ss = lse_parts->strides[1];
+  a.l_sh = lse_parts->strides[2];
+  a.num = static_cast<const int*>(num_parts->data);
+  a.num_s = num_parts->strides[0];
+  a.N = (int)N;
+  a.S = (int)S;
+  a.H = (int)H;
+  a.out = out->data;
+  a.out_f32 = out->dtype == RL_F32;
+  a.out_sn = out->strides[0];
+  a.out_sh = out->strides[1];
+  a.lse_out = lse_out ? static_cast<float*>(lse_out->data) : nullptr;
+  a.lo_sn = lse_out ? lse_out->strides[0] : 0;
+  a.lo_sh = lse_out ? lse_out->strides[1] : 0;
+  hipError_t e = rl::launch_merge(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
+  return RL_OK;
+}
+
+const char* rl_attn_last_error(void) { return g_err.c_str(); }
+
+int rl_attn_check_device_errors(void* stream) {
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Workspace* w = nullptr;
+  RL_TRY(acquire_ws(st, 0, &w));
+  hipError_t e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  int word = 0;
+  e = hipMemcpy(&word, w->err, sizeof(int), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy");
+  e = hipMemset(w->err, 0, sizeof(int));
+  if (e != hipSuccess) return hip_fail(e, "hipMemset");
+  if (word) {
+    std::string what;
+    if (word & rl::kErrLen) what += " length-out-of-range";
+    if (word & rl::kErrPage) what += " page-id-out-of-range";
+    if (word & rl::kErrIndptr) what += " qo_indptr-invalid";
+    if (word & rl::kErrKvShort) what += " kv_lens-shorter-than-chunk";
+    return fail(RL_ERR_DEVICE, "device-side input errors (values were clamped):%s", what.c_str());
+  }
+  return RL_OK;
+}
+
+int rl_attn_reserve_workspace(size_t bytes, void* stream) {
+  Workspace* w = nullptr;
+  return acquire_ws(static_cast<hipStream_t>(stream), bytes, &w);
+}
+
+size_t rl_attn_decode_workspace_size(int64_t batch, int64_t num_q_heads, int64_t num_kv_heads, int64_t max_pages,
+                                     int64_t page_size) {
+  if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0) return 0;
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) == hipSuccess) cus = device_cus(dev);
+  return decode_layout(batch, num_q_heads, num_kv_heads, max_pages, page_size, env().split_tokens, cus).total;
+}
+
+size_t rl_attn_extend_workspace_size(int64_t batch, int64_t total_q, int64_t num_q_heads, int64_t num_kv_heads,
+                                     int64_t max_pages, int64_t page_size) {
+  (void)max_pages;
+  (void)page_size;
+  if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0) return 0;
+  int mi = 0;
+  return extend_ws_bytes(batch, total_q, num_q_heads / num_kv_heads, &mi);
+}
+
+int rl_attn_profile_enable(int on) {
+  Profiler& p = prof();
+  std::lock_guard<std::mutex> lk(p.mu);
+  p.on = on != 0;
+  return RL_OK;
+}
+
+int rl_attn_profile_read(int kind, int* launches, double* mean_ms) {
+  if (kind != 0 && kind != 1) return fail(RL_ERR_INVALID_ARG, "kind must be 0 (decode) or 1 (extend)");
+  if (!launches || !mean_ms) return fail(RL_ERR_INVALID_ARG, "launches and mean_ms must not be NULL");
+  std::vector<rl::KernelTimer> ts;
+  {
+    Profiler& p = prof();
+    std::lock_guard<std::mutex> lk(p.mu);
+    ts.swap(p.pending[kind]);
+  }
+  double total = 0.0;
+  int n = 0;
+  int rc = RL_OK;
+  for (auto& t : ts) {
+    float ms = 0.f;
+    if (rc == RL_OK) {
+      hipError_t e = hipEventSynchronize(t.stop);
+      if (e == hipSuccess) e = hipEventElapsedTime(&ms, t.start, t.stop);
+      if (e != hipSuccess) rc = hip_fail(e, "hipEventElapsedTime");
+      total += ms;
+      ++n;
+    }
+    (void)hipEventDestroy(t.start);
+    (void)hipEventDestroy(t.stop);
+  }
+  *launches = n;
+  *mean_ms = n ? total / n : 0.0;
+  return rc;
+}
+
+void rl_attn_release(void) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  (void)hipDeviceSynchronize();
+  for (auto& kv : g_ws) {
+    if (kv.second.ptr) (void)hipFree(kv.second.ptr);
+    if (kv.second.err) (void)hipFree(kv.second.err);
+  }
+  g_ws.clear();
+}
+
+}  // extern "C"

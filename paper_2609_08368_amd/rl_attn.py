@@ -1,0 +1,213 @@
+"""Thin ctypes binding over librlattn.so (argument marshalling only).
+
+Every step of the attention runs in the HIP library; this module turns torch
+tensors into the ABI's non-owning ``rl_tensor`` views and passes torch's
+current stream. There is no fallback: if the library is missing or a call
+fails, an exception is raised.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "librlattn.so")
+HEADER = os.path.join(os.path.dirname(_PKG), "include", "rl_attn.h")
+
+RL_BF16, RL_F32, RL_I32 = 1, 2, 3
+RL_PREFIX_AUTO, RL_PREFIX_OFF = 0, 1
+STATUS = {
+    0: "RL_OK", -1: "RL_ERR_INVALID_ARG", -2: "RL_ERR_SHAPE", -3: "RL_ERR_DTYPE", -4: "RL_ERR_UNSUPPORTED",
+    -5: "RL_ERR_WORKSPACE", -6: "RL_ERR_HIP", -7: "RL_ERR_DEVICE",
+}
+CODES = {v: k for k, v in STATUS.items()}
+
+
+class RlTensor(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32),
+                ("shape", ctypes.c_int64 * 4), ("strides", ctypes.c_int64 * 4)]
+
+
+class RlOpts(ctypes.Structure):
+    _fields_ = [("split_tokens", ctypes.c_int32), ("prefix_share", ctypes.c_int32),
+                ("validate", ctypes.c_int32), ("reserved", ctypes.c_int32 * 5)]
+
+
+class RlAttnError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"{STATUS.get(code, code)}: {message}")
+        self.code = code
+        self.status = STATUS.get(code, str(code))
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load librlattn.so (built by ``python -m paper_2609_08368_amd.build``)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER(RlTensor)
+        vp = ctypes.c_void_p
+        L.rl_attn_decode.argtypes = [P, P, P, P, P, ctypes.c_float, P, vp]
+        L.rl_attn_extend.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, vp]
+        L.rl_attn_decode_ex.argtypes = [P, P, P, P, P, ctypes.c_float, P, P, ctypes.POINTER(RlOpts), vp]
+        L.rl_attn_extend_ex.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, P, ctypes.POINTER(RlOpts), vp]
+        L.rl_attn_merge.argtypes = [P, P, P, P, P, vp]
+        L.rl_attn_last_error.restype = ctypes.c_char_p
+        L.rl_attn_check_device_errors.argtypes = [vp]
+        L.rl_attn_reserve_workspace.argtypes = [ctypes.c_size_t, vp]
+        L.rl_attn_decode_workspace_size.argtypes = [ctypes.c_int64] * 5
+        L.rl_attn_decode_workspace_size.restype = ctypes.c_size_t
+        L.rl_attn_extend_workspace_size.argtypes = [ctypes.c_int64] * 6
+        L.rl_attn_extend_workspace_size.restype = ctypes.c_size_t
+        L.rl_attn_release.restype = None
+        L.rl_attn_profile_enable.argtypes = [ctypes.c_int]
+        L.rl_attn_profile_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double)]
+        for name in ("rl_attn_decode", "rl_attn_extend", "rl_attn_decode_ex", "rl_attn_extend_ex",
+                     "rl_attn_merge", "rl_attn_check_device_errors", "rl_attn_reserve_workspace",
+                     "rl_attn_profile_enable", "rl_attn_profile_read"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def header_functions() -> list:
+    """Names of the functions ``include/rl_attn.h`` declares."""
+    with open(HEADER) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rl_attn_\w+)\s*\(", text)))
+
+
+def last_error() -> str:
+    return lib().rl_attn_last_error().decode()
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise RlAttnError(rc, last_error())
+
+
+_DTYPES = {torch.bfloat16: RL_BF16, torch.float32: RL_F32, torch.int32: RL_I32}
+
+
+def view(t: Optional[torch.Tensor]):
+    """An ``rl_tensor`` describing ``t`` (no copy); None -> NULL."""
+    if t is None:
+        return None
+    if t.dim() > 4:
+        raise ValueError("rl_tensor holds at most 4 dimensions")
+    v = RlTensor()
+    v.data = t.data_ptr() if t.numel() else (t.data_ptr() or None)
+    v.dtype = _DTYPES.get(t.dtype, 0)
+    v.ndim = t.dim()
+    for i in range(t.dim()):
+        v.shape[i] = t.shape[i]
+        v.strides[i] = t.stride(i)
+    return v
+
+
+def _ref(v):
+    return ctypes.byref(v) if v is not None else None
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def _opts(split_tokens=0, prefix_share=True, validate=False):
+    o = RlOpts()
+    o.split_tokens = int(split_tokens)
+    o.prefix_share = RL_PREFIX_AUTO if prefix_share else RL_PREFIX_OFF
+    o.validate = int(bool(validate))
+    return o
+
+
+def decode(q, k_pages, v_pages, block_table, seq_lens, scale, out=None, lse=None, *, split_tokens=0,
+           prefix_share=True, validate=False, stream=None):
+    """``rl_attn_decode_ex``: returns ``out`` (and fills ``lse`` if given)."""
+    if out is None:
+        out = torch.empty_like(q)
+    o = _opts(split_tokens, prefix_share, validate)
+    _check(lib().rl_attn_decode_ex(_ref(view(q)), _ref(view(k_pages)), _ref(view(v_pages)),
+                                   _ref(view(block_table)), _ref(view(seq_lens)), ctypes.c_float(scale),
+                                   _ref(view(out)), _ref(view(lse)), ctypes.byref(o), _stream(stream)))
+    return out
+
+
+def decode_plain(q, k_pages, v_pages, block_table, seq_lens, scale, out=None, stream=None):
+    """``rl_attn_decode`` (the fixed signature, no options)."""
+    if out is None:
+        out = torch.empty_like(q)
+    _check(lib().rl_attn_decode(_ref(view(q)), _ref(view(k_pages)), _ref(view(v_pages)),
+                                _ref(view(block_table)), _ref(view(seq_lens)), ctypes.c_float(scale),
+                                _ref(view(out)), _stream(stream)))
+    return out
+
+
+def extend(q, qo_indptr, k_pages, v_pages, block_table, kv_lens, scale, out=None, lse=None, *,
+           validate=False, stream=None):
+    """``rl_attn_extend_ex``: returns ``out`` (and fills ``lse`` if given)."""
+    if out is None:
+        out = torch.empty_like(q)
+    o = _opts(0, True, validate)
+    _check(lib().rl_attn_extend_ex(_ref(view(q)), _ref(view(qo_indptr)), _ref(view(k_pages)),
+                                   _ref(view(v_pages)), _ref(view(block_table)), _ref(view(kv_lens)),
+                                   ctypes.c_float(scale), _ref(view(out)), _ref(view(lse)), ctypes.byref(o),
+                                   _stream(stream)))
+    return out
+
+
+def extend_plain(q, qo_indptr, k_pages, v_pages, block_table, kv_lens, scale, out=None, stream=None):
+    """``rl_attn_extend`` (the fixed signature)."""
+    if out is None:
+        out = torch.empty_like(q)
+    _check(lib().rl_attn_extend(_ref(view(q)), _ref(view(qo_indptr)), _ref(view(k_pages)), _ref(view(v_pages)),
+                                _ref(view(block_table)), _ref(view(kv_lens)), ctypes.c_float(scale),
+                                _ref(view(out)), _stream(stream)))
+    return out
+
+
+def merge(o_parts, lse_parts, num_parts, out=None, lse=None, stream=None):
+    """``rl_attn_merge``: log-sum-exp merge of partial results."""
+    n, _, h, d = o_parts.shape
+    if out is None:
+        out = torch.empty((n, h, d), dtype=torch.float32, device=o_parts.device)
+    _check(lib().rl_attn_merge(_ref(view(o_parts)), _ref(view(lse_parts)), _ref(view(num_parts)),
+                               _ref(view(out)), _ref(view(lse)), _stream(stream)))
+    return out
+
+
+def check_device_errors(stream=None):
+    _check(lib().rl_attn_check_device_errors(_stream(stream)))
+
+
+def reserve_workspace(nbytes: int, stream=None):
+    _check(lib().rl_attn_reserve_workspace(ctypes.c_size_t(nbytes), _stream(stream)))
+
+
+def profile_enable(on: bool = True):
+    _check(lib().rl_attn_profile_enable(int(bool(on))))
+
+
+def profile_read(kind: str):
+    """(launches, mean ms) of the main kernel timed since the last read; kind 'decode' or 'extend'."""
+    n = ctypes.c_int()
+    ms = ctypes.c_double()
+    _check(lib().rl_attn_profile_read({"decode": 0, "extend": 1}[kind], ctypes.byref(n), ctypes.byref(ms)))
+    return n.value, ms.value
+
+
+def release():
+    lib().rl_attn_release()

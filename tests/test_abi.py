@@ -1,0 +1,148 @@
+"""C-ABI library: loads, exports every declared symbol, rejects bad arguments
+before touching the GPU (CPU only; no compute calls)."""
+
+import ctypes
+
+import pytest
+import torch
+
+from paper_2609_08368_amd import rl_attn as ra
+
+FAKE = 0x100000          # never dereferenced: every call below fails host validation first
+
+
+def fake(shape, dtype, ptr=FAKE, strides=None):
+    v = ra.RlTensor()
+    v.data = ptr
+    v.dtype = dtype
+    v.ndim = len(shape)
+    st = strides
+    if st is None:
+        st, acc = [], 1
+        for s in reversed(shape):
+            st.insert(0, acc)
+            acc *= s
+    for i, s in enumerate(shape):
+        v.shape[i] = s
+        v.strides[i] = st[i]
+    return v
+
+
+def decode_args(B=2, Hq=8, Hkv=2, P=16, npages=10, maxp=4, D=128):
+    return dict(
+        q=fake([B, Hq, D], ra.RL_BF16), k=fake([npages, P, Hkv, D], ra.RL_BF16),
+        v=fake([npages, P, Hkv, D], ra.RL_BF16), bt=fake([B, maxp], ra.RL_I32),
+        lens=fake([B], ra.RL_I32), out=fake([B, Hq, D], ra.RL_BF16), lse=None, opts=None)
+
+
+def call_decode(a):
+    r = ctypes.byref
+    return ra.lib().rl_attn_decode_ex(r(a["q"]), r(a["k"]), r(a["v"]), r(a["bt"]), r(a["lens"]),
+                                      ctypes.c_float(0.088), r(a["out"]),
+                                      r(a["lse"]) if a["lse"] is not None else None,
+                                      r(a["opts"]) if a["opts"] is not None else None, None)
+
+
+def test_library_exports_every_declared_symbol():
+    names = ra.header_functions()
+    assert {"rl_attn_decode", "rl_attn_extend", "rl_attn_merge", "rl_attn_last_error"} <= set(names)
+    lib = ra.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+@pytest.mark.parametrize("mutate,code,needle", [
+    (lambda a: a.update(q=None) or a, "RL_ERR_INVALID_ARG", "q is NULL"),
+    (lambda a: setattr(a["q"], "dtype", ra.RL_F32) or a, "RL_ERR_DTYPE", "q must be bf16"),
+    (lambda a: a.update(q=fake([2, 8], ra.RL_BF16)) or a, "RL_ERR_SHAPE", "q must have 3"),
+    (lambda a: a.update(**decode_args(D=64)) or a, "RL_ERR_UNSUPPORTED", "head dimension must be 128"),
+    (lambda a: a.update(**decode_args(P=48)) or a, "RL_ERR_UNSUPPORTED", "page size"),
+    (lambda a: a.update(**decode_args(P=256)) or a, "RL_ERR_UNSUPPORTED", "page size"),
+    (lambda a: a.update(**decode_args(P=4)) or a, "RL_ERR_UNSUPPORTED", "page size"),
+    (lambda a: a.update(**decode_args(Hq=6, Hkv=4)) or a, "RL_ERR_SHAPE", "multiple of KV heads"),
+    (lambda a: a.update(bt=fake([3, 4], ra.RL_I32)) or a, "RL_ERR_SHAPE", "block_table.shape[0]"),
+    (lambda a: a.update(bt=fake([2, 4], ra.RL_F32)) or a, "RL_ERR_DTYPE", "block_table must be int32"),
+    (lambda a: a.update(lens=fake([3], ra.RL_I32)) or a, "RL_ERR_SHAPE", "seq_lens.shape[0]"),
+    (lambda a: a.update(lens=fake([2], ra.RL_F32)) or a, "RL_ERR_DTYPE", "seq_lens must be int32"),
+    (lambda a: a.update(out=fake([2, 8, 128], ra.RL_I32)) or a, "RL_ERR_DTYPE", "out must be bf16 or f32"),
+    (lambda a: a.update(out=fake([2, 4, 128], ra.RL_BF16)) or a, "RL_ERR_SHAPE", "out shape"),
+    (lambda a: a.update(lse=fake([2, 7], ra.RL_F32)) or a, "RL_ERR_SHAPE", "lse_out shape"),
+    (lambda a: a.update(lse=fake([2, 8], ra.RL_BF16)) or a, "RL_ERR_DTYPE", "lse_out must be f32"),
+    (lambda a: a.update(k=fake([10, 16, 2, 128], ra.RL_BF16, strides=[4096, 256, 128, 2])) or a,
+     "RL_ERR_UNSUPPORTED", "last stride"),
+    (lambda a: a.update(q=fake([2, 8, 128], ra.RL_BF16, ptr=FAKE + 2)) or a, "RL_ERR_UNSUPPORTED", "aligned"),
+    (lambda a: a.update(v=fake([10, 16, 2, 128], ra.RL_BF16, ptr=0)) or a, "RL_ERR_INVALID_ARG", "v_pages.data"),
+    (lambda a: a.update(v=fake([11, 16, 2, 128], ra.RL_BF16)) or a, "RL_ERR_SHAPE", "shapes differ"),
+])
+def test_decode_validation(mutate, code, needle):
+    a = mutate(decode_args())
+    if a["q"] is None:
+        rc = ra.lib().rl_attn_decode_ex(None, ctypes.byref(a["k"]), ctypes.byref(a["v"]), ctypes.byref(a["bt"]),
+                                        ctypes.byref(a["lens"]), ctypes.c_float(1.0), ctypes.byref(a["out"]),
+                                        None, None, None)
+    else:
+        rc = call_decode(a)
+    assert ra.STATUS[rc] == code, ra.last_error()
+    assert needle in ra.last_error()
+
+
+@pytest.mark.parametrize("field,value,needle", [
+    ("split_tokens", 100, "split_tokens"), ("split_tokens", -64, "split_tokens"),
+    ("prefix_share", 7, "prefix_share"), ("validate", 2, "validate")])
+def test_option_validation(field, value, needle):
+    a = decode_args()
+    o = ra.RlOpts()
+    setattr(o, field, value)
+    a["opts"] = o
+    assert ra.STATUS[call_decode(a)] == "RL_ERR_INVALID_ARG"
+    assert needle in ra.last_error()
+    o2 = ra.RlOpts()
+    o2.reserved[3] = 1
+    a["opts"] = o2
+    assert ra.STATUS[call_decode(a)] == "RL_ERR_INVALID_ARG" and "reserved" in ra.last_error()
+
+
+def test_empty_batch_is_a_no_op():
+    a = decode_args(B=0)
+    assert call_decode(a) == 0
+
+
+def test_extend_validation():
+    r = ctypes.byref
+    B = 3
+    q = fake([10, 8, 128], ra.RL_BF16)
+    k = fake([20, 16, 2, 128], ra.RL_BF16)
+    bt = fake([B, 4], ra.RL_I32)
+    kv = fake([B], ra.RL_I32)
+    out = fake([10, 8, 128], ra.RL_BF16)
+    bad_indptr = fake([B], ra.RL_I32)
+    rc = ra.lib().rl_attn_extend(r(q), r(bad_indptr), r(k), r(k), r(bt), r(kv), ctypes.c_float(1.0), r(out), None)
+    assert ra.STATUS[rc] == "RL_ERR_SHAPE" and "qo_indptr" in ra.last_error()
+    indptr = fake([B + 1], ra.RL_F32)
+    rc = ra.lib().rl_attn_extend(r(q), r(indptr), r(k), r(k), r(bt), r(kv), ctypes.c_float(1.0), r(out), None)
+    assert ra.STATUS[rc] == "RL_ERR_DTYPE"
+    indptr = fake([B + 1], ra.RL_I32)
+    out_bad = fake([9, 8, 128], ra.RL_BF16)
+    rc = ra.lib().rl_attn_extend(r(q), r(indptr), r(k), r(k), r(bt), r(kv), ctypes.c_float(1.0), r(out_bad), None)
+    assert ra.STATUS[rc] == "RL_ERR_SHAPE"
+    q0 = fake([0, 8, 128], ra.RL_BF16)
+    out0 = fake([0, 8, 128], ra.RL_BF16)
+    rc = ra.lib().rl_attn_extend(r(q0), r(indptr), r(k), r(k), r(bt), r(kv), ctypes.c_float(1.0), r(out0), None)
+    assert rc == 0, ra.last_error()
+
+
+def test_merge_validation():
+    r = ctypes.byref
+    o = fake([4, 3, 8, 128], ra.RL_F32)
+    l = fake([4, 3, 8], ra.RL_F32)
+    n = fake([4], ra.RL_I32)
+    out = fake([4, 8, 128], ra.RL_F32)
+    assert ra.STATUS[ra.lib().rl_attn_merge(r(o), r(fake([4, 2, 8], ra.RL_F32)), r(n), r(out), None, None)] == "RL_ERR_SHAPE"
+    assert ra.STATUS[ra.lib().rl_attn_merge(r(o), r(l), r(fake([4], ra.RL_F32)), r(out), None, None)] == "RL_ERR_DTYPE"
+    assert ra.STATUS[ra.lib().rl_attn_merge(r(fake([4, 3, 8, 64], ra.RL_F32)), r(l), r(n), r(fake([4, 8, 64], ra.RL_F32)), None, None)] == "RL_ERR_UNSUPPORTED"
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="checks the no-GPU error path")
+def test_valid_call_without_gpu_reports_hip_error():
+    rc = call_decode(decode_args())
+    assert ra.STATUS[rc] in ("RL_ERR_HIP", "RL_ERR_WORKSPACE"), ra.last_error()
