@@ -28,7 +28,8 @@
  *
  * Tensors: every argument is a non-owning view. dtype/ndim/shape are checked
  * on the host; strides are in elements and free except that the last (head
- * dimension) stride must be 1. All pointers are device pointers on the
+ * dimension) stride must be 1 (page strides below 2^32 elements, slot strides
+ * and block-table column strides below 2^24). All pointers are device pointers on the
  * current HIP device. The library only reads q, pages, tables and lengths and
  * only writes out / lse_out. Head dimension must be 128; Hq % Hkv == 0;
  * page size P must be a power of two in [8, 128].
@@ -97,7 +98,7 @@ typedef struct {
  *   v_pages     same shape and dtype as k_pages
  *   block_table [B, max_pages] int32 (entries past ceil(seq_lens[b]/P) are never read)
  *   seq_lens    [B] int32, 0 <= seq_lens[b] <= max_pages * P
- *   scale       softmax scale (e.g. 1/sqrt(128))
+ *   scale       softmax scale (e.g. 1/sqrt(128)); must be positive and finite
  *   out         [B, Hq, 128] bf16 (f32 also accepted), written
  * Returns RL_OK or an RL_ERR_* code. */
 int rl_attn_decode(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages,

@@ -58,15 +58,49 @@ __device__ __forceinline__ bf16x8 load_bf16x8(const __bf16* p) {
 
 __device__ __forceinline__ __bf16 bits_to_bf16(u16 b) { return __builtin_bit_cast(__bf16, b); }
 
-// Page id of logical token t, clamped into the pool (a bad id is recorded in *bad).
-__device__ __forceinline__ int64_t page_of(const int* bt_row, int64_t bt_sj, int t, int log2p, int num_pages,
-                                           int* bad) {
-  int pg = bt_row[(int64_t)(t >> log2p) * bt_sj];
+// Page id of logical token t, clamped into the pool (a bad id is recorded in
+// *bad). The host guarantees that block-table column strides and indices fit
+// 24 bits, so the index is a single 24-bit multiply.
+__device__ __forceinline__ uint32_t page_of(const int* bt_row, uint32_t bt_sj, int t, int log2p, int num_pages,
+                                            int* bad) {
+  int pg = bt_row[__umul24((uint32_t)(t >> log2p), bt_sj)];
   if ((unsigned)pg >= (unsigned)num_pages) {
     *bad = 1;
     pg = pg < 0 ? 0 : num_pages - 1;
   }
-  return pg;
+  return (uint32_t)pg;
+}
+
+// Element offset of (page, slot) inside a page pool: the page stride fits 32
+// bits and the slot stride 24 bits (host-checked), so this is one 32x32->64
+// multiply-add plus one 24-bit multiply.
+__device__ __forceinline__ uint64_t row_offset(uint32_t pg, uint32_t sp, int slot, uint32_t ss) {
+  return (uint64_t)pg * sp + __umul24((uint32_t)slot, ss);
+}
+
+// Exclusive prefix sum over the calling block (all threads must call it);
+// wave_tot is a 16-int LDS scratch array. Returns this thread's exclusive sum
+// and the block total in *total.
+__device__ __forceinline__ int block_exclusive_scan(int v, int* total, int* wave_tot) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wave_tot[wave] = x;
+  __syncthreads();
+  int before = 0, all = 0;
+  const int nw = blockDim.x >> 6;
+  for (int w = 0; w < nw; ++w) {
+    int t = wave_tot[w];
+    if (w < wave) before += t;
+    all += t;
+  }
+  __syncthreads();
+  *total = all;
+  return before + x - v;
 }
 
 }  // namespace rl

@@ -1,45 +1,35 @@
-// Batched paged decode: device planner, split-KV attention, log-sum-exp combine.
+// Batched paged decode: device planner, split-KV attention, trajectory-group
+// prefix pass, log-sum-exp combine.
 //
-// One work item is (sequence b, split s): keys [s*C, min(L_b, (s+1)*C)) of one
-// sequence. The planner runs on the device from the lengths alone, so the host
-// never waits for data: it picks C so that the number of work items stays
-// near a target, and records, per sequence, how many splits it has.
-// A sequence with one split writes its final output directly; longer ones
-// write per-split (o, lse) partials that the combine kernel merges
-// (flash-decoding; the merge rule is the log-sum-exp identity).
-#include "attn_common.hpp"
+// The planner runs on the device from the lengths and the block table, so the
+// host never waits for data. It
+//   * picks the split size C (a multiple of 64 keys) so that the number of
+//     work items stays near a target;
+//   * finds trajectory groups: sequences whose block tables start with the
+//     same page id form a group with its lowest-indexed member as leader, and
+//     share the leading full pages they have in common with the leader (the
+//     minimum over the group). The G attempts at one prompt are scheduled
+//     together and reuse the prompt's cached prefix (paper, sections "The
+//     Miles RL Loop" and "Fast Agentic Rollout with SGLang"), so their block
+//     tables point at the same physical pages;
+//   * emits shared items (a split of a group's shared keys, computed once for
+//     up to 128 query rows of every member) and private items (a split of the
+//     rest of one sequence).
+// A sequence whose whole context is one private item writes its output
+// directly; otherwise every item writes an (o, lse) partial into a slot of the
+// sequence and the combine kernel merges them (flash-decoding; the merge is the
+// log-sum-exp identity).
 #include "kernels.hpp"
+#include "tile_attn.hpp"
 
 namespace rl {
 
 namespace {
 
-constexpr int kMinSplit = 256;     // smallest automatic split (tokens)
-constexpr int kTile = 32;          // keys per inner iteration
-
-// Exclusive prefix sum over a 1024-thread block; returns the block total in *total.
-__device__ int block_exclusive_scan(int v, int* total) {
-  __shared__ int wave_tot[16];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) wave_tot[wave] = x;
-  __syncthreads();
-  int before = 0, all = 0;
-  const int nw = blockDim.x >> 6;
-  for (int w = 0; w < nw; ++w) {
-    int t = wave_tot[w];
-    if (w < wave) before += t;
-    all += t;
-  }
-  __syncthreads();
-  *total = all;
-  return before + x - v;
-}
+constexpr int kMinSplit = 256;     // smallest automatic split (keys)
+constexpr int kTile = 32;          // keys per inner iteration of the private kernel
+constexpr int kGroupMax = 1024;    // batches up to this size get trajectory-group detection
+constexpr int kIntMax = 0x7fffffff;
 
 __device__ __forceinline__ int clamp_len(int L, int max_tokens, int* bad) {
   if (L < 0 || L > max_tokens) {
@@ -49,20 +39,38 @@ __device__ __forceinline__ int clamp_len(int L, int max_tokens, int* bad) {
   return L;
 }
 
+__device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
 __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
-  const int tid = threadIdx.x;
-  const int max_tokens = a.kv.max_pages * a.kv.page_size;
-  int bad = 0;
-  long long sum = 0;
-  for (int b = tid; b < a.B; b += blockDim.x) sum += clamp_len(a.lens[b * a.lens_s], max_tokens, &bad);
-  // block sum of the lengths
+  __shared__ int sL[kGroupMax], sP0[kGroupMax], sLead[kGroupMax], sKmin[kGroupMax], sCnt[kGroupMax],
+      sSg[kGroupMax];
+  __shared__ int wave_tot[16];
   __shared__ long long wsum[16];
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int lg = a.kv.log2_page, P = a.kv.page_size;
+  const int max_tokens = a.kv.max_pages * P;
+  const bool grouping = a.group_cap >= 2 && a.B <= kGroupMax;
+  const uint32_t bt_sj = (uint32_t)a.kv.bt_sj;
+  int bad = 0;
+
+  // lengths, their sum, and each sequence's first page id (when it has a full page)
+  long long sum = 0;
+  for (int b = tid; b < a.B; b += nthr) {
+    const int L = clamp_len(a.lens[b * a.lens_s], max_tokens, &bad);
+    sum += L;
+    if (grouping) {
+      sL[b] = L;
+      sP0[b] = (L >> lg) > 0 ? a.kv.bt[(int64_t)b * a.kv.bt_sb] : -1 - b;
+      sKmin[b] = kIntMax;
+      sCnt[b] = 0;
+    }
+  }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
   if ((tid & 63) == 0) wsum[tid >> 6] = sum;
   __syncthreads();
   long long total = 0;
-  for (int w = 0; w < (int)(blockDim.x >> 6); ++w) total += wsum[w];
+  for (int w = 0; w < (nthr >> 6); ++w) total += wsum[w];
 
   int C = a.forced_split;
   if (C <= 0) {
@@ -70,38 +78,138 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
     per = (per + 63) & ~63LL;
     C = (int)(per < kMinSplit ? kMinSplit : per);
   }
-  int offset = 0;
-  for (int b0 = 0; b0 < a.B; b0 += blockDim.x) {
+
+  if (grouping) {
+    // leader = lowest-indexed sequence with the same first page id
+    for (int b = tid; b < a.B; b += nthr) {
+      int lead = b;
+      const int key = sP0[b];
+      if (key >= 0)
+        for (int j = 0; j < b; ++j)
+          if (sP0[j] == key) {
+            lead = j;
+            break;
+          }
+      sLead[b] = lead;
+    }
+    __syncthreads();
+    // leading full pages each member shares with its leader; the group shares the minimum
+    for (int b = tid; b < a.B; b += nthr) {
+      const int lead = sLead[b];
+      if (lead == b) continue;
+      const int lim = min(sL[b], sL[lead]) >> lg;
+      const int* rb = a.kv.bt + (int64_t)b * a.kv.bt_sb;
+      const int* rl = a.kv.bt + (int64_t)lead * a.kv.bt_sb;
+      int k = 0;
+      while (k < lim && rb[__umul24((uint32_t)k, bt_sj)] == rl[__umul24((uint32_t)k, bt_sj)]) ++k;
+      atomicMin(&sKmin[lead], k);
+      atomicAdd(&sCnt[lead], 1);
+    }
+    __syncthreads();
+  }
+  // a sequence shares with its group when the group has another member and at least one full page
+  auto shared_keys = [&](int b) -> int {
+    if (!grouping) return 0;
+    const int lead = sLead[b];
+    return (sCnt[lead] >= 1 && sKmin[lead] >= 1) ? sKmin[lead] * P : 0;
+  };
+  const int cap = a.group_cap;
+
+  // sub-groups of at most `cap` members: bases by an exclusive scan over leaders
+  int n_sg = 0;
+  if (grouping) {
+    const int b = tid;
+    int nsub = 0;
+    if (b < a.B && sLead[b] == b && shared_keys(b) > 0) nsub = ceil_div(sCnt[b] + 1, cap);
+    const int excl = block_exclusive_scan(nsub, &n_sg, wave_tot);
+    if (b < a.B) sSg[b] = excl;
+    __syncthreads();
+  }
+
+  // per sequence: slots, private items, sub-group membership
+  int slot_off = 0, item_off = 0;
+  for (int b0 = 0; b0 < a.B; b0 += nthr) {
     const int b = b0 + tid;
-    int ns = 0;
+    int L = 0, S = 0, nsh = 0, npriv = 0, nslots = 0;
+    bool direct = false;
     if (b < a.B) {
       int dummy = 0;
-      const int L = clamp_len(a.lens[b * a.lens_s], max_tokens, &dummy);
-      ns = L > 0 ? (L + C - 1) / C : 1;
+      L = grouping ? sL[b] : clamp_len(a.lens[b * a.lens_s], max_tokens, &dummy);
+      S = shared_keys(b);
+      const int priv = L - S;
+      nsh = S > 0 ? ceil_div(S, C) : 0;
+      npriv = priv > 0 ? ceil_div(priv, C) : (S > 0 ? 0 : 1);
+      direct = S == 0 && npriv == 1;
+      nslots = direct ? 0 : nsh + npriv;
     }
-    int chunk_total;
-    const int excl = block_exclusive_scan(ns, &chunk_total);
+    int slot_tot, item_tot;
+    const int slot_base = slot_off + block_exclusive_scan(nslots, &slot_tot, wave_tot);
+    const int item_base = item_off + block_exclusive_scan(npriv, &item_tot, wave_tot);
     if (b < a.B) {
-      const int first = offset + excl;
-      a.ws.nsplit[b] = ns;
-      a.ws.base[b] = first;
-      for (int s = 0; s < ns; ++s)
-        if (first + s < a.max_items) a.ws.items[first + s] = make_int2(b, s);
+      a.ws.nparts[b] = slot_base + nslots <= a.max_slots ? nslots : 0;
+      a.ws.base[b] = slot_base;
+      for (int s = 0; s < npriv; ++s) {
+        const int idx = item_base + s;
+        const int t0 = S + s * C;
+        const int slot = direct ? -1 : slot_base + nsh + s;
+        if (idx < a.max_items && slot < a.max_slots) a.ws.items[idx] = make_int4(b, t0, min(L, t0 + C), slot);
+      }
+      if (S > 0) {
+        const int lead = sLead[b];
+        int rank = 0;
+        if (b != lead)
+          for (int j = lead + 1; j <= b; ++j) rank += sLead[j] == lead;
+        const int sg = sSg[lead] + rank / cap, pos = rank % cap;
+        a.ws.sg_members[sg * cap + pos] = b;
+        if (pos == 0) a.ws.sgroups[sg] = make_int4(b, min(cap, sCnt[lead] + 1 - (rank / cap) * cap), S, nsh);
+      }
     }
-    offset += chunk_total;
+    slot_off += slot_tot;
+    item_off += item_tot;
+  }
+  __syncthreads();
+
+  // shared items: the splits of each sub-group's shared keys
+  int sitem_off = 0;
+  for (int g0 = 0; g0 < n_sg; g0 += nthr) {
+    const int sg = g0 + tid;
+    int4 info = make_int4(0, 0, 0, 0);
+    if (sg < n_sg) info = a.ws.sgroups[sg];
+    int tot;
+    const int base = sitem_off + block_exclusive_scan(sg < n_sg ? info.w : 0, &tot, wave_tot);
+    if (sg < n_sg)
+      for (int s = 0; s < info.w; ++s)
+        if (base + s < a.max_items) a.ws.sitems[base + s] = make_int4(sg, s * C, min(info.z, (s + 1) * C), s);
+    sitem_off += tot;
   }
   if (tid == 0) {
     a.ws.hdr[0] = C;
-    a.ws.hdr[1] = offset < a.max_items ? offset : a.max_items;
+    a.ws.hdr[1] = min(item_off, a.max_items);
+    a.ws.hdr[2] = min(sitem_off, a.max_items);
+    a.ws.hdr[3] = n_sg;
   }
   if (bad) atomicOr(a.ws.err, kErrLen);
 }
 
+// Writes a finished (o, l, m) for one query head: directly to out/lse, or as
+// a normalised partial into a slot.
+struct HeadResult {
+  float inv, lse;
+};
+
+__device__ __forceinline__ HeadResult finish(float m_log2, float l) {
+  HeadResult r;
+  r.inv = l > 0.f ? 1.f / l : 0.f;
+  r.lse = l > 0.f ? (m_log2 + __builtin_amdgcn_logf(l)) * kLn2 : kNegInf;
+  return r;
+}
+
 // Split-KV decode on MFMA for a packed GQA group of up to 16 query heads.
-// One wave per (work item, KV head, 16-head block). Keys are processed 32 at a
-// time: K goes straight from HBM into A-operand registers (each lane loads
-// 4 x 16 contiguous bytes of one key row), V is staged in LDS and read back
-// transposed as the A operand of O^T += V^T P^T.
+// One wave per (private item, KV head, 16-head block). Keys are processed 32
+// at a time: K goes straight from HBM into A-operand registers (each lane
+// loads 4 x 16 contiguous bytes of one key row), V is staged in LDS and read
+// back transposed as the A operand of O^T += V^T P^T. Page ids are loaded one
+// tile ahead of the rows they address.
 __global__ __launch_bounds__(64) void decode_mfma_kernel(DecodeArgs a) {
   __shared__ u16 vs[kTile][kHeadDim + 8];
 
@@ -112,14 +220,9 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DecodeArgs a) {
   const int g = rem % a.Hkv;
   const int qb = rem / a.Hkv;
   if (item >= a.ws.hdr[1]) return;
-  const int2 it = a.ws.items[item];
-  const int b = it.x, s = it.y;
-  const int C = a.ws.hdr[0];
-  const int max_tokens = a.kv.max_pages * a.kv.page_size;
+  const int4 it = a.ws.items[item];
+  const int b = it.x, t_begin = it.y, t_end = it.z, slot = it.w;
   int bad = 0;
-  const int L = clamp_len(a.lens[b * a.lens_s], max_tokens, &bad);
-  const int t_begin = s * C;
-  const int t_end = min(L, t_begin + C);
 
   const int lane = threadIdx.x;
   const int col = lane & 15, grp = lane >> 4;
@@ -142,20 +245,38 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DecodeArgs a) {
   const float sl2 = a.scale * kLog2e;
 
   const int* bt_row = a.kv.bt + (int64_t)b * a.kv.bt_sb;
+  const uint32_t bt_sj = (uint32_t)a.kv.bt_sj;
   const __bf16* kbase = (const __bf16*)a.kv.k + (int64_t)g * a.kv.sh + grp * 8;
   const __bf16* vbase = (const __bf16*)a.kv.v + (int64_t)g * a.kv.v_sh + grp * 8;
+  const uint32_t ksp = (uint32_t)a.kv.sp, kss = (uint32_t)a.kv.ss;
+  const uint32_t vsp = (uint32_t)a.kv.v_sp, vss = (uint32_t)a.kv.v_ss;
+  const int pmask = a.kv.page_size - 1;
+  // tiles start at multiples of 32 keys, so a page of >= 32 keys holds a whole tile
+  const bool page_holds_tile = a.kv.page_size >= kTile && (t_begin & (kTile - 1)) == 0;
 
   if (t_begin < t_end) {
     bf16x8 kc[2][4], vc[2][4];
-    auto load_tile = [&](int t0) {
+    int praw[2];
+    auto fetch_pages = [&](int t0) {
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        int t = t0 + (page_holds_tile ? 0 : 16 * hh + col);
+        t = t < t_end ? t : t_end - 1;
+        praw[hh] = (page_holds_tile && hh) ? 0 : bt_row[__umul24((uint32_t)(t >> a.kv.log2_page), bt_sj)];
+      }
+    };
+    auto fetch_rows = [&](int t0) {
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
         int t = t0 + 16 * hh + col;
         t = t < t_end ? t : t_end - 1;
-        const int64_t pg = page_of(bt_row, a.kv.bt_sj, t, a.kv.log2_page, a.kv.num_pages, &bad);
-        const int slot = t & (a.kv.page_size - 1);
-        const __bf16* kp = kbase + pg * a.kv.sp + (int64_t)slot * a.kv.ss;
-        const __bf16* vp = vbase + pg * a.kv.v_sp + (int64_t)slot * a.kv.v_ss;
+        int pg = praw[page_holds_tile ? 0 : hh];
+        if ((unsigned)pg >= (unsigned)a.kv.num_pages) {
+          bad = 1;
+          pg = pg < 0 ? 0 : a.kv.num_pages - 1;
+        }
+        const __bf16* kp = kbase + row_offset((uint32_t)pg, ksp, t & pmask, kss);
+        const __bf16* vp = vbase + row_offset((uint32_t)pg, vsp, t & pmask, vss);
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           kc[hh][c] = load_bf16x8(kp + c * 32);
@@ -163,7 +284,9 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DecodeArgs a) {
         }
       }
     };
-    load_tile(t_begin);
+    fetch_pages(t_begin);
+    fetch_rows(t_begin);
+    if (t_begin + kTile < t_end) fetch_pages(t_begin + kTile);
     for (int t0 = t_begin; t0 < t_end; t0 += kTile) {
       __syncthreads();  // previous tile's V reads are done
 #pragma unroll
@@ -173,32 +296,34 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DecodeArgs a) {
           *reinterpret_cast<bf16x8*>(&vs[16 * hh + col][c * 32 + grp * 8]) = vc[hh][c];
       f32x4 st[2];
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        st[hh] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int hh = 0; hh < 2; ++hh) st[hh] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int c = 0; c < 4; ++c) st[hh] = mfma_16x16x32(kc[hh][c], qv[c], st[hh]);
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) st[hh] = mfma_16x16x32(kc[hh][c], qv[c], st[hh]);
+      if (t0 + kTile < t_end) {
+        fetch_rows(t0 + kTile);
+        if (t0 + 2 * kTile < t_end) fetch_pages(t0 + 2 * kTile);
       }
-      if (t0 + kTile < t_end) load_tile(t0 + kTile);
 
-      float sv[8];
       float mt = kNegInf;
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int t = t0 + 16 * hh + 4 * grp + i;
-          const float x = t < t_end ? st[hh][i] * sl2 : kNegInf;
-          sv[hh * 4 + i] = x;
-          mt = fmaxf(mt, x);
+          if (t >= t_end) st[hh][i] = kNegInf;
+          mt = fmaxf(mt, st[hh][i]);
         }
-      mt = group_max(mt);
+      mt = group_max(mt) * sl2;
       const float m_new = fmaxf(m_run, mt);
       const float alpha = exp2_fast(m_run - m_new);
+      const float neg_m = -m_new;
       float ps = 0.f;
       bf16x8 pb;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float p = exp2_fast(sv[e] - m_new);
+        const float p = exp2_fast(fmaf(st[e >> 2][e & 3], sl2, neg_m));
         ps += p;
         pb[e] = (__bf16)p;
       }
@@ -220,32 +345,30 @@ __global__ __launch_bounds__(64) void decode_mfma_kernel(DecodeArgs a) {
     }
   }
 
-  const float l_tot = group_sum(l_run);
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  const float lse_v = l_tot > 0.f ? (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2 : kNegInf;
+  const HeadResult res = finish(m_run, group_sum(l_run));
   if (col_ok) {
-    if (a.ws.nsplit[b] == 1) {
+    if (slot < 0) {
       if (a.out_f32) {
         float* op = (float*)a.out + (int64_t)b * a.out_sb + (int64_t)h * a.out_sh + 4 * grp;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) *reinterpret_cast<f32x4*>(op + 16 * j) = o[j] * inv;
+        for (int j = 0; j < 8; ++j) *reinterpret_cast<f32x4*>(op + 16 * j) = o[j] * res.inv;
       } else {
+        typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
         __bf16* op = (__bf16*)a.out + (int64_t)b * a.out_sb + (int64_t)h * a.out_sh + 4 * grp;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
           bf16x4 w;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) w[i] = (__bf16)(o[j][i] * inv);
+          for (int i = 0; i < 4; ++i) w[i] = (__bf16)(o[j][i] * res.inv);
           *reinterpret_cast<bf16x4*>(op + 16 * j) = w;
         }
       }
-      if (a.lse && grp == 0) a.lse[(int64_t)b * a.lse_sb + (int64_t)h * a.lse_sh] = lse_v;
+      if (a.lse && grp == 0) a.lse[(int64_t)b * a.lse_sb + (int64_t)h * a.lse_sh] = res.lse;
     } else {
-      float* pp = a.ws.part_o + ((int64_t)item * a.Hq + h) * kHeadDim + 4 * grp;
+      float* pp = a.ws.part_o + ((int64_t)slot * a.Hq + h) * kHeadDim + 4 * grp;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) *reinterpret_cast<f32x4*>(pp + 16 * j) = o[j] * inv;
-      if (grp == 0) a.ws.part_lse[(int64_t)item * a.Hq + h] = lse_v;
+      for (int j = 0; j < 8; ++j) *reinterpret_cast<f32x4*>(pp + 16 * j) = o[j] * res.inv;
+      if (grp == 0) a.ws.part_lse[(int64_t)slot * a.Hq + h] = res.lse;
     }
   }
   if (bad) atomicOr(a.ws.err, kErrPage);
@@ -258,14 +381,9 @@ __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
   const int item = blockIdx.x / a.Hkv;
   const int g = blockIdx.x - item * a.Hkv;
   if (item >= a.ws.hdr[1]) return;
-  const int2 it = a.ws.items[item];
-  const int b = it.x, s = it.y;
-  const int C = a.ws.hdr[0];
-  const int max_tokens = a.kv.max_pages * a.kv.page_size;
+  const int4 it = a.ws.items[item];
+  const int b = it.x, t_begin = it.y, t_end = it.z, slot = it.w;
   int bad = 0;
-  const int L = clamp_len(a.lens[b * a.lens_s], max_tokens, &bad);
-  const int t_begin = s * C;
-  const int t_end = min(L, t_begin + C);
   const int lane = threadIdx.x;
   const int c16 = lane & 15, grp = lane >> 4;
   const int h = g;  // R == 1
@@ -281,16 +399,17 @@ __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = 0.f;
   const int* bt_row = a.kv.bt + (int64_t)b * a.kv.bt_sb;
+  const uint32_t bt_sj = (uint32_t)a.kv.bt_sj;
   const __bf16* kbase = (const __bf16*)a.kv.k + (int64_t)g * a.kv.sh + c16 * 8;
   const __bf16* vbase = (const __bf16*)a.kv.v + (int64_t)g * a.kv.v_sh + c16 * 8;
   for (int t0 = t_begin; t0 < t_end; t0 += 4) {
     const int t = t0 + grp;
     const bool valid = t < t_end;
     const int tt = valid ? t : t_end - 1;
-    const int64_t pg = page_of(bt_row, a.kv.bt_sj, tt, a.kv.log2_page, a.kv.num_pages, &bad);
-    const int slot = tt & (a.kv.page_size - 1);
-    const bf16x8 kk = load_bf16x8(kbase + pg * a.kv.sp + (int64_t)slot * a.kv.ss);
-    const bf16x8 vv = load_bf16x8(vbase + pg * a.kv.v_sp + (int64_t)slot * a.kv.v_ss);
+    const uint32_t pg = page_of(bt_row, bt_sj, tt, a.kv.log2_page, a.kv.num_pages, &bad);
+    const int slot_t = tt & (a.kv.page_size - 1);
+    const bf16x8 kk = load_bf16x8(kbase + row_offset(pg, (uint32_t)a.kv.sp, slot_t, (uint32_t)a.kv.ss));
+    const bf16x8 vv = load_bf16x8(vbase + row_offset(pg, (uint32_t)a.kv.v_sp, slot_t, (uint32_t)a.kv.v_ss));
     float d = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) d += qf[i] * (float)kk[i];
@@ -313,33 +432,73 @@ __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
   const float l_tot = group_sum(l * w);
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = group_sum(acc[i] * w);
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  const float lse_v = l_tot > 0.f ? (M + __builtin_amdgcn_logf(l_tot)) * kLn2 : kNegInf;
+  const HeadResult res = finish(M, l_tot);
   if (grp == 0) {
-    if (a.ws.nsplit[b] == 1) {
+    if (slot < 0) {
       if (a.out_f32) {
         float* op = (float*)a.out + (int64_t)b * a.out_sb + (int64_t)h * a.out_sh + c16 * 8;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) op[i] = acc[i] * inv;
+        for (int i = 0; i < 8; ++i) op[i] = acc[i] * res.inv;
       } else {
         bf16x8 w8;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) w8[i] = (__bf16)(acc[i] * inv);
+        for (int i = 0; i < 8; ++i) w8[i] = (__bf16)(acc[i] * res.inv);
         *reinterpret_cast<bf16x8*>((__bf16*)a.out + (int64_t)b * a.out_sb + (int64_t)h * a.out_sh + c16 * 8) = w8;
       }
-      if (a.lse && c16 == 0) a.lse[(int64_t)b * a.lse_sb + (int64_t)h * a.lse_sh] = lse_v;
+      if (a.lse && c16 == 0) a.lse[(int64_t)b * a.lse_sb + (int64_t)h * a.lse_sh] = res.lse;
     } else {
-      float* pp = a.ws.part_o + ((int64_t)item * a.Hq + h) * kHeadDim + c16 * 8;
+      float* pp = a.ws.part_o + ((int64_t)slot * a.Hq + h) * kHeadDim + c16 * 8;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) pp[i] = acc[i] * inv;
-      if (c16 == 0) a.ws.part_lse[(int64_t)item * a.Hq + h] = lse_v;
+      for (int i = 0; i < 8; ++i) pp[i] = acc[i] * res.inv;
+      if (c16 == 0) a.ws.part_lse[(int64_t)slot * a.Hq + h] = res.lse;
     }
   }
   if (bad) atomicOr(a.ws.err, kErrPage);
 }
 
-// Merge the split partials of one (sequence, query head): one wave, two
-// output elements per lane.
+// Group-prefix pass: one workgroup per (shared item, KV head) computes the
+// shared keys of a sub-group once for all its members' query rows (row r ->
+// member r / R, query head r % R), reading each shared page once, and writes
+// one partial per member into that member's slot for this split.
+__global__ __launch_bounds__(256, 2) void prefix_kernel(DecodeArgs a) {
+  __shared__ TileLds lds;
+  const int item = blockIdx.x / a.Hkv;
+  const int g = blockIdx.x - item * a.Hkv;
+  if (item >= a.ws.hdr[2]) return;
+  const int4 it = a.ws.sitems[item];
+  const int sg = it.x, t0 = it.y, t1 = it.z, split = it.w;
+  const int4 info = a.ws.sgroups[sg];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = wave * kWaveRows + (lane & 31);
+  const int member = r / a.R, hi = r - member * a.R;
+  const bool row_ok = member < info.y;
+  const int b = a.ws.sg_members[sg * a.group_cap + (row_ok ? member : 0)];
+  const int head = g * a.R + hi;
+
+  bf16x8 qv[8];
+  load_q_operand((const __bf16*)a.q + (int64_t)b * a.q_sb + (int64_t)head * a.q_sh, row_ok, qv);
+  f32x16 o[4];
+#pragma unroll
+  for (int jd = 0; jd < 4; ++jd)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[jd][e] = 0.f;
+  float m_run = kNegInf, l_run = 0.f;
+  int bad = 0;
+  tile_attend(a.kv, a.scale, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g, t0, t1, t1, t1 - 1, qv, lds, o, m_run,
+              l_run, bad);
+  const HeadResult res = finish(m_run, l_run + __shfl_xor(l_run, 32, 64));
+  if (row_ok) {
+    const int slot = a.ws.base[b] + split;
+    if (slot < a.max_slots) {
+      store_o_row(a.ws.part_o + ((int64_t)slot * a.Hq + head) * kHeadDim, o, res.inv);
+      if (lane < 32) a.ws.part_lse[(int64_t)slot * a.Hq + head] = res.lse;
+    }
+  }
+  if (bad) atomicOr(a.ws.err, kErrPage);
+}
+
+// Merge the partials of one (sequence, query head): one wave, two output
+// elements per lane.
 __device__ __forceinline__ void merge_parts(const float* o_base, int64_t o_step, const float* l_base, int64_t l_step,
                                             int n, float* out2, float* lse_out) {
   const int lane = threadIdx.x;
@@ -365,13 +524,12 @@ __device__ __forceinline__ void merge_parts(const float* o_base, int64_t o_step,
 __global__ __launch_bounds__(64) void combine_kernel(DecodeArgs a) {
   const int b = blockIdx.x / a.Hq;
   const int h = blockIdx.x - b * a.Hq;
-  const int ns = a.ws.nsplit[b];
-  if (ns <= 1) return;
+  const int n = a.ws.nparts[b];
+  if (n <= 0) return;
   const int base = a.ws.base[b];
-  if (base + ns > a.max_items) return;  // cannot happen for consistent plans
   float r[2], lse_v;
   merge_parts(a.ws.part_o + ((int64_t)base * a.Hq + h) * kHeadDim, (int64_t)a.Hq * kHeadDim,
-              a.ws.part_lse + (int64_t)base * a.Hq + h, a.Hq, ns, r, &lse_v);
+              a.ws.part_lse + (int64_t)base * a.Hq + h, a.Hq, n, r, &lse_v);
   const int lane = threadIdx.x;
   if (a.out_f32) {
     float* op = (float*)a.out + (int64_t)b * a.out_sb + (int64_t)h * a.out_sh + 2 * lane;
@@ -412,6 +570,7 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream, KernelTimer* t
   plan_decode_kernel<<<1, 1024, 0, stream>>>(a);
   const unsigned per_item = a.R == 1 ? a.Hkv : a.Hkv * ((a.R + 15) / 16);
   const unsigned grid = (unsigned)a.max_items * per_item;
+  if (a.group_cap >= 2) prefix_kernel<<<(unsigned)a.max_items * a.Hkv, kTileWaves * 64, 0, stream>>>(a);
   if (timer) (void)hipEventRecord(timer->start, stream);
   if (a.R == 1)
     decode_valu_kernel<<<grid, 64, 0, stream>>>(a);

@@ -25,14 +25,21 @@ struct PagedKV {
   int num_pages, page_size, log2_page, max_pages;
 };
 
-// Workspace carve-up of one decode or extend call.
+// Workspace carve-up of one decode call. Work items: private items cover a
+// key range of one sequence; shared items cover the prefix pages a trajectory
+// group shares and serve every member of one sub-group (at most 128 query
+// rows). Partial results live in "slots"; sequence b owns slots
+// base[b] .. base[b] + nparts[b] - 1 (nparts[b] == 0: written directly).
 struct DecodePlanWs {
-  int* hdr;        // [0] split tokens, [1] number of work items
-  int* nsplit;     // [B]
-  int* base;       // [B] first work item of each sequence
-  int2* items;     // [max_items] (sequence, split index)
-  float* part_o;   // [max_items, Hq, 128]
-  float* part_lse; // [max_items, Hq]
+  int* hdr;        // [0] split tokens C, [1] private items, [2] shared items, [3] sub-groups
+  int* nparts;     // [B]
+  int* base;       // [B]
+  int4* items;     // [max_items] (sequence, first key, end key, slot or -1 for a direct write)
+  int4* sitems;    // [max_items] (sub-group, first key, end key, split index)
+  int4* sgroups;   // [B] (sequence whose block table is read, members, shared keys, shared splits)
+  int* sg_members; // [B * group_cap] member sequences of each sub-group
+  float* part_o;   // [max_slots, Hq, 128]
+  float* part_lse; // [max_slots, Hq]
   int* err;        // device error word (persistent)
 };
 
@@ -51,15 +58,16 @@ struct DecodeArgs {
   int64_t lse_sb, lse_sh;
   int forced_split;       // 0 = choose on device
   int target_items;       // work items the device planner aims for
-  int max_items;          // capacity of the item list / partial buffers
-  int prefix_share;       // 1 = read group-shared prefix pages once per group
+  int max_items;          // capacity of each item list
+  int max_slots;          // capacity of the partial buffers
+  int group_cap;          // members per sub-group (128 query rows / R), 0 = no prefix sharing
   int validate;
   DecodePlanWs ws;
 };
 
 struct ExtendPlanWs {
-  int* hdr;        // [0] number of q tiles
-  int4* items;     // [max_items] (sequence, first chunk row, rows, key limit base)
+  int* hdr;        // [0] number of work units
+  int4* items;     // [max_items] (sequence, first chunk row, chunk rows, KV head | head block << 16)
   int* err;
 };
 

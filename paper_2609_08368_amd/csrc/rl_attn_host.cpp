@@ -131,6 +131,14 @@ int check_rows128(const rl_tensor* t, const char* name) {
   return RL_OK;
 }
 
+// The kernels take the row maximum of raw scores and fold the scale into the
+// exponent, which needs a positive, finite scale.
+int check_scale(float scale) {
+  if (!(scale > 0.f) || !std::isfinite(scale))
+    return fail(RL_ERR_INVALID_ARG, "scale must be positive and finite (got %g)", (double)scale);
+  return RL_OK;
+}
+
 #define RL_TRY(x)          \
   do {                     \
     int rc_ = (x);         \
@@ -236,41 +244,53 @@ void prof_commit(int kind, rl::KernelTimer* t) {
 }
 
 // ------------------------------------------------------------------- decode
+// Capacities (see the planner): with split size C and T = sum(L) / C,
+// private items <= T + B, shared items <= T + B, partial slots <= T + 2B.
+// An automatic C keeps T at or below the target item count; a forced C
+// bounds T by B * ceil(max_pages * P / C).
 struct DecodeLayout {
-  int max_items;
-  size_t off_nsplit, off_base, off_items, off_po, off_pl, total;
+  int max_items, max_slots, group_cap;
+  size_t off_nparts, off_base, off_items, off_sitems, off_sgroups, off_members, off_po, off_pl, total;
 };
 
-DecodeLayout decode_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t max_pages, int64_t P, int split, int cus) {
+int64_t decode_wgs_per_item(int64_t Hq, int64_t Hkv) {
+  const int64_t R = Hq / std::max<int64_t>(1, Hkv);
+  return Hkv * (R == 1 ? 1 : (R + 15) / 16);
+}
+
+int target_items_for(int64_t Hq, int64_t Hkv, int cus) {
+  return (int)std::max<int64_t>(1, (int64_t)cus * env().target_wgs_per_cu / decode_wgs_per_item(Hq, Hkv));
+}
+
+DecodeLayout decode_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t max_pages, int64_t P, int split, int cus,
+                           bool prefix_share) {
   DecodeLayout L{};
   const int64_t R = Hq / std::max<int64_t>(1, Hkv);
-  const int64_t per_item = Hkv * (R == 1 ? 1 : (R + 15) / 16);
   const int64_t max_tokens = max_pages * P;
-  int64_t items;
-  if (split > 0)
-    items = B * std::max<int64_t>(1, (max_tokens + split - 1) / split);
-  else
-    items = B + std::max<int64_t>(1, (int64_t)cus * env().target_wgs_per_cu / std::max<int64_t>(1, per_item));
-  L.max_items = (int)std::min<int64_t>(items, INT32_MAX / 2);
+  const int64_t T = split > 0 ? B * std::max<int64_t>(1, (max_tokens + split - 1) / split)
+                              : (int64_t)target_items_for(Hq, Hkv, cus);
+  L.max_items = (int)std::min<int64_t>(T + B, INT32_MAX / 2);
+  L.max_slots = (int)std::min<int64_t>(T + 2 * B, INT32_MAX / 2);
+  L.group_cap = (prefix_share && R <= 64) ? (int)(128 / R) : 0;
   size_t off = 256;  // header
-  L.off_nsplit = off;
+  L.off_nparts = off;
   off += align256(B * 4);
   L.off_base = off;
   off += align256(B * 4);
   L.off_items = off;
-  off += align256((size_t)L.max_items * 8);
+  off += align256((size_t)L.max_items * 16);
+  L.off_sitems = off;
+  off += align256((size_t)L.max_items * 16);
+  L.off_sgroups = off;
+  off += align256((size_t)B * 16);
+  L.off_members = off;
+  off += align256((size_t)B * std::max(1, L.group_cap) * 4);
   L.off_po = off;
-  off += align256((size_t)L.max_items * Hq * 128 * 4);
+  off += align256((size_t)L.max_slots * Hq * 128 * 4);
   L.off_pl = off;
-  off += align256((size_t)L.max_items * Hq * 4);
+  off += align256((size_t)L.max_slots * Hq * 4);
   L.total = off;
   return L;
-}
-
-int target_items_for(int64_t Hq, int64_t Hkv, int cus) {
-  const int64_t R = Hq / Hkv;
-  const int64_t per_item = Hkv * (R == 1 ? 1 : (R + 15) / 16);
-  return (int)std::max<int64_t>(1, (int64_t)cus * env().target_wgs_per_cu / per_item);
 }
 
 int fill_paged(const rl_tensor* k, const rl_tensor* v, const rl_tensor* bt, int64_t B, rl::PagedKV* kv) {
@@ -292,6 +312,13 @@ int fill_paged(const rl_tensor* k, const rl_tensor* v, const rl_tensor* bt, int6
   if (k->shape[0] < 1 && bt->shape[1] > 0) return fail(RL_ERR_SHAPE, "the page pool is empty");
   if (k->shape[0] > INT32_MAX || bt->shape[1] * P > INT32_MAX)
     return fail(RL_ERR_UNSUPPORTED, "page pool or block table too large for 32-bit token indices");
+  // index arithmetic on the device: page strides fit 32 bits, slot strides,
+  // block-table column strides and page indices fit 24 bits
+  const int64_t lim32 = (int64_t)1 << 32, lim24 = (int64_t)1 << 24;
+  if (k->strides[0] >= lim32 || v->strides[0] >= lim32 || k->strides[1] >= lim24 || v->strides[1] >= lim24)
+    return fail(RL_ERR_UNSUPPORTED, "k_pages/v_pages: page stride must be < 2^32 and slot stride < 2^24 elements");
+  if (bt->strides[1] < 0 || bt->strides[1] >= lim24 || bt->shape[1] >= lim24 || bt->strides[0] < 0)
+    return fail(RL_ERR_UNSUPPORTED, "block_table: column stride and width must be < 2^24, strides non-negative");
   RL_TRY(check_data(k, "k_pages"));
   RL_TRY(check_data(v, "v_pages"));
   RL_TRY(check_data(bt, "block_table"));
@@ -341,6 +368,7 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
                 void* stream) {
   Opts o;
   RL_TRY(read_opts(opts, &o));
+  RL_TRY(check_scale(scale));
   RL_TRY(check_view(q, "q", 3));
   RL_TRY(check_dtype(q, "q", RL_BF16));
   RL_TRY(check_rows128(q, "q"));
@@ -367,7 +395,8 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   const int cus = device_cus(dev);
-  const DecodeLayout lay = decode_layout(B, Hq, Hkv, a.kv.max_pages, a.kv.page_size, o.split_tokens, cus);
+  const DecodeLayout lay = decode_layout(B, Hq, Hkv, a.kv.max_pages, a.kv.page_size, o.split_tokens, cus,
+                                         o.prefix_share == RL_PREFIX_AUTO);
   Workspace* w = nullptr;
   RL_TRY(acquire_ws(st, lay.total, &w));
   char* base = static_cast<char*>(w->ptr);
@@ -391,12 +420,16 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   a.forced_split = o.split_tokens;
   a.target_items = target_items_for(Hq, Hkv, cus);
   a.max_items = lay.max_items;
-  a.prefix_share = o.prefix_share == RL_PREFIX_AUTO;
+  a.max_slots = lay.max_slots;
+  a.group_cap = lay.group_cap;
   a.validate = o.validate;
   a.ws.hdr = reinterpret_cast<int*>(base);
-  a.ws.nsplit = reinterpret_cast<int*>(base + lay.off_nsplit);
+  a.ws.nparts = reinterpret_cast<int*>(base + lay.off_nparts);
   a.ws.base = reinterpret_cast<int*>(base + lay.off_base);
-  a.ws.items = reinterpret_cast<int2*>(base + lay.off_items);
+  a.ws.items = reinterpret_cast<int4*>(base + lay.off_items);
+  a.ws.sitems = reinterpret_cast<int4*>(base + lay.off_sitems);
+  a.ws.sgroups = reinterpret_cast<int4*>(base + lay.off_sgroups);
+  a.ws.sg_members = reinterpret_cast<int*>(base + lay.off_members);
   a.ws.part_o = reinterpret_cast<float*>(base + lay.off_po);
   a.ws.part_lse = reinterpret_cast<float*>(base + lay.off_pl);
   a.ws.err = w->err;
@@ -421,9 +454,11 @@ ExtendShape extend_shape(int64_t R) {
   return s;
 }
 
-size_t extend_ws_bytes(int64_t B, int64_t total_q, int64_t R, int* max_items) {
+// Work units are (sequence, KV head, head block, chunk tile): at most
+// Hkv * head_blocks * (B + ceil(total_q / tile_tokens)).
+size_t extend_ws_bytes(int64_t B, int64_t total_q, int64_t Hkv, int64_t R, int* max_items) {
   const ExtendShape s = extend_shape(R);
-  const int64_t items = B + (total_q + s.tile_tokens - 1) / s.tile_tokens;
+  const int64_t items = Hkv * s.head_blocks * (B + (total_q + s.tile_tokens - 1) / s.tile_tokens);
   *max_items = (int)std::min<int64_t>(items, INT32_MAX / 2);
   return 256 + align256((size_t)*max_items * 16);
 }
@@ -433,6 +468,7 @@ int extend_impl(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor*
                 rl_tensor* lse_out, const rl_attn_opts* opts, void* stream) {
   Opts o;
   RL_TRY(read_opts(opts, &o));
+  RL_TRY(check_scale(scale));
   RL_TRY(check_view(q, "q", 3));
   RL_TRY(check_dtype(q, "q", RL_BF16));
   RL_TRY(check_rows128(q, "q"));
@@ -463,7 +499,7 @@ int extend_impl(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor*
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   int max_items = 0;
-  const size_t bytes = extend_ws_bytes(B, total_q, Hq / Hkv, &max_items);
+  const size_t bytes = extend_ws_bytes(B, total_q, Hkv, Hq / Hkv, &max_items);
   Workspace* w = nullptr;
   RL_TRY(acquire_ws(st, bytes, &w));
   char* base = static_cast<char*>(w->ptr);
@@ -620,7 +656,9 @@ size_t rl_attn_decode_workspace_size(int64_t batch, int64_t num_q_heads, int64_t
   if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0) return 0;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess) cus = device_cus(dev);
-  return decode_layout(batch, num_q_heads, num_kv_heads, max_pages, page_size, env().split_tokens, cus).total;
+  return decode_layout(batch, num_q_heads, num_kv_heads, max_pages, page_size, env().split_tokens, cus,
+                       env().prefix_share == RL_PREFIX_AUTO)
+      .total;
 }
 
 size_t rl_attn_extend_workspace_size(int64_t batch, int64_t total_q, int64_t num_q_heads, int64_t num_kv_heads,
@@ -629,7 +667,7 @@ size_t rl_attn_extend_workspace_size(int64_t batch, int64_t total_q, int64_t num
   (void)page_size;
   if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0) return 0;
   int mi = 0;
-  return extend_ws_bytes(batch, total_q, num_q_heads / num_kv_heads, &mi);
+  return extend_ws_bytes(batch, total_q, num_kv_heads, num_q_heads / num_kv_heads, &mi);
 }
 
 int rl_attn_profile_enable(int on) {

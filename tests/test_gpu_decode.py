@@ -134,3 +134,45 @@ def test_decode_full_size_sampled(name):
     H.say(f"  {name} rows={rows} {res}")
     del t
     torch.cuda.empty_cache()
+
+
+PREFIX_CASES = [
+    # (page_size, Hq, Hkv, group_size, groups, shared_tokens, private lens, split)
+    (16, 8, 2, 4, 3, 64, [5, 40, 0, 17], 0),            # a member with no private keys
+    (16, 8, 2, 4, 2, 60, [1, 30, 70, 2], 64),           # shared prefix not page aligned: 3 full pages
+    (64, 64, 8, 8, 2, 4096, [512, 700, 1000, 64, 3, 200, 900, 513], 0),
+    (64, 64, 8, 8, 2, 4096, [512, 700, 1000, 64, 3, 200, 900, 513], 1024),
+    (32, 16, 1, 20, 1, 256, list(range(1, 21)), 128),   # 20 members x 16 rows: two sub-groups
+    (16, 2, 2, 3, 2, 48, [10, 0, 5], 0),                 # one query head per KV head
+]
+
+
+@pytest.mark.parametrize("case", PREFIX_CASES, ids=[f"P{c[0]}_h{c[1]}kv{c[2]}_G{c[3]}_s{c[7]}" for c in PREFIX_CASES])
+@pytest.mark.parametrize("share", [True, False])
+def test_decode_group_prefix_sharing(case, share):
+    ps, hq, hkv, gs, ng, shared, priv, split = case
+    lens = [shared + priv[j % len(priv)] + 7 * g for g in range(ng) for j in range(gs)]
+    w = wl.custom(50 + gs, "decode", lens, hq=hq, hkv=hkv, page_size=ps, group_size=gs, shared_tokens=shared)
+    H.say(f"prefix case {case} share={share}")
+    t = wl.materialize(w, DEV)
+    out, lse = H.run_decode(w, t, split_tokens=split, prefix_share=share)
+    ref_o, ref_l = H.oracle_full(w, t)
+    H.compare(out, ref_o, lse, ref_l, what=f"{case} share={share}")
+
+
+def test_decode_group_prefix_shuffled_batch():
+    """Groups scattered over the batch (shuffled order) are still found; results match the oracle."""
+    w = wl.decode_group_prefix(shuffle=True)
+    H.say("group prefix, shuffled batch")
+    t = wl.materialize(w, DEV)
+    out, lse = H.run_decode(w, t)
+    out_off, lse_off = H.run_decode(w, t, prefix_share=False)
+    assert torch.isfinite(out.float()).all()
+    rows = [0, 1, 17, 64, 127]
+    ref_o, ref_l = H.oracle_decode_rows(w, t, rows)
+    sel = torch.tensor(rows, device=DEV)
+    H.compare(out[sel], ref_o, lse[sel], ref_l, what="shuffled shared")
+    H.compare(out_off[sel], ref_o, lse_off[sel], ref_l, what="shuffled unshared")
+    # both runs agree with each other everywhere at the path's tolerance (each is a
+    # bf16-rounded result, so they differ by up to twice the per-side error)
+    H.compare(out, H.f64(out_off), what="shared vs unshared")
