@@ -30,6 +30,7 @@ constexpr int kMinSplit = 256;     // smallest automatic split (keys)
 constexpr int kTile = 32;          // keys per inner iteration of the private kernel
 constexpr int kGroupMax = 1024;    // batches up to this size get trajectory-group detection
 constexpr int kIntMax = 0x7fffffff;
+constexpr int kXcds = 8;
 
 __device__ __forceinline__ int clamp_len(int L, int max_tokens, int* bad) {
   if (L < 0 || L > max_tokens) {
@@ -210,21 +211,34 @@ __device__ __forceinline__ HeadResult finish(float m_log2, float l) {
 // loads 4 x 16 contiguous bytes of one key row), V is staged in LDS and read
 // back transposed as the A operand of O^T += V^T P^T. Page ids are loaded one
 // tile ahead of the rows they address.
-__global__ __launch_bounds__(64) void decode_mfma_kernel(DecodeArgs a) {
-  __shared__ u16 vs[kTile][kHeadDim + 8];
+__global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
+  // one V tile per wave (dynamic LDS: the workgroup's waves x 32 keys x 272 B)
+  extern __shared__ u16 vs_dyn[];
+  typedef u16 VTile[kTile][kHeadDim + 8];
 
   const int nqb = (a.R + 15) >> 4;
   const int per_item = a.Hkv * nqb;
-  const int item = blockIdx.x / per_item;
-  const int rem = blockIdx.x - item * per_item;
+  const int wpg = a.item_waves;             // waves per workgroup; divides per_item
+  const int nch = per_item / wpg;
+  // Workgroup x runs on XCD x % 8; give each XCD a contiguous range of
+  // (item, wave group) pairs.
+  const int total = a.ws.hdr[1] * nch;
+  const int per_xcd = (total + kXcds - 1) / kXcds;
+  const int jx = blockIdx.x / kXcds;
+  if (jx >= per_xcd) return;
+  const int lin = (blockIdx.x % kXcds) * per_xcd + jx;
+  if (lin >= total) return;
+  const int item = lin / nch;
+  const int wave = threadIdx.x >> 6;
+  const int rem = (lin - item * nch) * wpg + wave;
+  VTile& vs = reinterpret_cast<VTile*>(vs_dyn)[wave];
   const int g = rem % a.Hkv;
   const int qb = rem / a.Hkv;
-  if (item >= a.ws.hdr[1]) return;
   const int4 it = a.ws.items[item];
   const int b = it.x, t_begin = it.y, t_end = it.z, slot = it.w;
   int bad = 0;
 
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int row0 = qb * 16;
   const int nrows = min(16, a.R - row0);
@@ -462,58 +476,86 @@ __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
 // one partial per member into that member's slot for this split.
 __global__ __launch_bounds__(256, 2) void prefix_kernel(DecodeArgs a) {
   __shared__ TileLds lds;
-  const int item = blockIdx.x / a.Hkv;
-  const int g = blockIdx.x - item * a.Hkv;
-  if (item >= a.ws.hdr[2]) return;
-  const int4 it = a.ws.sitems[item];
-  const int sg = it.x, t0 = it.y, t1 = it.z, split = it.w;
-  const int4 info = a.ws.sgroups[sg];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r = wave * kWaveRows + (lane & 31);
-  const int member = r / a.R, hi = r - member * a.R;
-  const bool row_ok = member < info.y;
-  const int b = a.ws.sg_members[sg * a.group_cap + (row_ok ? member : 0)];
-  const int head = g * a.R + hi;
+  // grid-stride over (shared item, KV head): a batch without trajectory groups
+  // costs one small launch that exits at once
+  const int n_work = a.ws.hdr[2] * a.Hkv;
+  for (int wi = blockIdx.x; wi < n_work; wi += gridDim.x) {
+    const int item = wi / a.Hkv;
+    const int g = wi - item * a.Hkv;
+    const int4 it = a.ws.sitems[item];
+    const int sg = it.x, t0 = it.y, t1 = it.z, split = it.w;
+    const int4 info = a.ws.sgroups[sg];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = wave * kWaveRows + (lane & 31);
+    const int member = r / a.R, hi = r - member * a.R;
+    const bool row_ok = member < info.y;
+    const int b = a.ws.sg_members[sg * a.group_cap + (row_ok ? member : 0)];
+    const int head = g * a.R + hi;
 
-  bf16x8 qv[8];
-  load_q_operand((const __bf16*)a.q + (int64_t)b * a.q_sb + (int64_t)head * a.q_sh, row_ok, qv);
-  f32x16 o[4];
+    bf16x8 qv[8];
+    load_q_operand((const __bf16*)a.q + (int64_t)b * a.q_sb + (int64_t)head * a.q_sh, row_ok, qv);
+    f32x16 o[4];
 #pragma unroll
-  for (int jd = 0; jd < 4; ++jd)
+    for (int jd = 0; jd < 4; ++jd)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) o[jd][e] = 0.f;
-  float m_run = kNegInf, l_run = 0.f;
-  int bad = 0;
-  tile_attend(a.kv, a.scale, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g, t0, t1, t1, t1 - 1, qv, lds, o, m_run,
-              l_run, bad);
-  const HeadResult res = finish(m_run, l_run + __shfl_xor(l_run, 32, 64));
-  if (row_ok) {
-    const int slot = a.ws.base[b] + split;
-    if (slot < a.max_slots) {
-      store_o_row(a.ws.part_o + ((int64_t)slot * a.Hq + head) * kHeadDim, o, res.inv);
-      if (lane < 32) a.ws.part_lse[(int64_t)slot * a.Hq + head] = res.lse;
+      for (int e = 0; e < 16; ++e) o[jd][e] = 0.f;
+    float m_run = kNegInf, l_run = 0.f;
+    int bad = 0;
+    tile_attend(a.kv, a.scale, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g, t0, t1, t1, t1 - 1, qv, lds, o, m_run,
+                l_run, bad);
+    const HeadResult res = finish(m_run, l_run + __shfl_xor(l_run, 32, 64));
+    if (row_ok) {
+      const int slot = a.ws.base[b] + split;
+      if (slot < a.max_slots) {
+        store_o_row(a.ws.part_o + ((int64_t)slot * a.Hq + head) * kHeadDim, o, res.inv);
+        if (lane < 32) a.ws.part_lse[(int64_t)slot * a.Hq + head] = res.lse;
+      }
     }
+    if (bad) atomicOr(a.ws.err, kErrPage);
+    __syncthreads();  // the LDS tiles are reused by the next work unit
   }
-  if (bad) atomicOr(a.ws.err, kErrPage);
 }
 
 // Merge the partials of one (sequence, query head): one wave, two output
-// elements per lane.
+// elements per lane. The lanes load the parts' log-sum-exps in parallel and
+// reduce them with cross-lane operations; the weighted sum over parts then
+// streams the partial outputs with independent loads.
 __device__ __forceinline__ void merge_parts(const float* o_base, int64_t o_step, const float* l_base, int64_t l_step,
                                             int n, float* out2, float* lse_out) {
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;
   float M = kNegInf;
-  for (int s = 0; s < n; ++s) M = fmaxf(M, l_base[s * l_step]);
+  for (int s0 = 0; s0 < n; s0 += 64)
+    if (s0 + lane < n) M = fmaxf(M, l_base[(int64_t)(s0 + lane) * l_step]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
   float z = 0.f, a0 = 0.f, a1 = 0.f;
   if (M != kNegInf) {
-    for (int s = 0; s < n; ++s) {
-      const float ls = l_base[s * l_step];
-      const float w = exp2_fast((ls - M) * kLog2e);
-      const float2 v = *reinterpret_cast<const float2*>(o_base + s * o_step + 2 * lane);
-      z += w;
-      a0 += w * v.x;
-      a1 += w * v.y;
+    for (int s0 = 0; s0 < n; s0 += 64) {
+      const float my_w = s0 + lane < n ? exp2_fast((l_base[(int64_t)(s0 + lane) * l_step] - M) * kLog2e) : 0.f;
+      z += my_w;
+      const int cnt = min(64, n - s0);
+      int s = 0;
+      for (; s + 4 <= cnt; s += 4) {
+        float2 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          v[u] = *reinterpret_cast<const float2*>(o_base + (int64_t)(s0 + s + u) * o_step + 2 * lane);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float w = __shfl(my_w, s + u, 64);
+          a0 += w * v[u].x;
+          a1 += w * v[u].y;
+        }
+      }
+      for (; s < cnt; ++s) {
+        const float2 v = *reinterpret_cast<const float2*>(o_base + (int64_t)(s0 + s) * o_step + 2 * lane);
+        const float w = __shfl(my_w, s, 64);
+        a0 += w * v.x;
+        a1 += w * v.y;
+      }
     }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) z += __shfl_xor(z, o, 64);
   }
   const float inv = z > 0.f ? 1.f / z : 0.f;
   out2[0] = a0 * inv;
@@ -569,13 +611,16 @@ __global__ __launch_bounds__(64) void merge_kernel(MergeArgs a) {
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream, KernelTimer* timer) {
   plan_decode_kernel<<<1, 1024, 0, stream>>>(a);
   const unsigned per_item = a.R == 1 ? a.Hkv : a.Hkv * ((a.R + 15) / 16);
-  const unsigned grid = (unsigned)a.max_items * per_item;
-  if (a.group_cap >= 2) prefix_kernel<<<(unsigned)a.max_items * a.Hkv, kTileWaves * 64, 0, stream>>>(a);
+  if (a.group_cap >= 2) prefix_kernel<<<(unsigned)a.prefix_grid, kTileWaves * 64, 0, stream>>>(a);
   if (timer) (void)hipEventRecord(timer->start, stream);
-  if (a.R == 1)
-    decode_valu_kernel<<<grid, 64, 0, stream>>>(a);
-  else
-    decode_mfma_kernel<<<grid, 64, 0, stream>>>(a);
+  if (a.R == 1) {
+    decode_valu_kernel<<<(unsigned)a.max_items * per_item, 64, 0, stream>>>(a);
+  } else {
+    const unsigned nch = per_item / a.item_waves;
+    const unsigned grid = (unsigned)(((int64_t)a.max_items * nch + kXcds - 1) / kXcds * kXcds);
+    const size_t lds = (size_t)a.item_waves * kTile * (kHeadDim + 8) * sizeof(u16);
+    decode_mfma_kernel<<<grid, 64 * a.item_waves, lds, stream>>>(a);
+  }
   if (timer) (void)hipEventRecord(timer->stop, stream);
   combine_kernel<<<(unsigned)(a.B * a.Hq), 64, 0, stream>>>(a);
   return hipGetLastError();

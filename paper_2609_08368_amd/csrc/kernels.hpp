@@ -61,6 +61,8 @@ struct DecodeArgs {
   int max_items;          // capacity of each item list
   int max_slots;          // capacity of the partial buffers
   int group_cap;          // members per sub-group (128 query rows / R), 0 = no prefix sharing
+  int prefix_grid;        // workgroups of the group-prefix pass (grid-stride over its work)
+  int item_waves;         // waves per decode workgroup: a divisor of Hkv * ceil(R / 16), at most 8
   int validate;
   DecodePlanWs ws;
 };

@@ -422,6 +422,17 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   a.max_items = lay.max_items;
   a.max_slots = lay.max_slots;
   a.group_cap = lay.group_cap;
+  a.prefix_grid = 2 * cus;
+  {
+    // the waves of one work item (its KV heads and 16-head blocks) share a workgroup
+    const int per_item = (int)(Hkv * ((a.R + 15) / 16));
+    a.item_waves = 1;
+    for (int w = std::min(per_item, 8); w >= 1; --w)
+      if (per_item % w == 0) {
+        a.item_waves = w;
+        break;
+      }
+  }
   a.validate = o.validate;
   a.ws.hdr = reinterpret_cast<int*>(base);
   a.ws.nparts = reinterpret_cast<int*>(base + lay.off_nparts);
