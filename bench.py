@@ -61,6 +61,101 @@ def cpu_baseline(w, tensors, budget_s: float):
                       f"({done_tokens} keys, {kv_bytes / 1e9:.2f} GB of KV) in {elapsed:.1f} s"}
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_ragged64k_hbm_traffic.json")
+CALIB_BYTES = 2 << 30   # bytes read and bytes written by the calibration copy
+
+
+def kernel_source_hash() -> str:
+    """Hash of the HIP sources the decode kernel is built from."""
+    import hashlib
+
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_08368_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".hpp", ".cpp")):
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def pmc_workload():
+    """What the counter runs profile: three ragged-64K decode calls and three
+    copies of CALIB_BYTES (the calibration kernel for FETCH_SIZE / WRITE_SIZE)."""
+    import torch
+
+    from paper_2609_08368_amd import rl_attn as ra
+    from paper_2609_08368_amd import workloads as wl
+
+    dev = torch.device("cuda:0")
+    w = wl.decode_ragged()
+    t = wl.materialize(w, dev, poison=False)
+    out = torch.empty_like(t["q"])
+    for _ in range(3):
+        ra.decode_plain(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out)
+    src = torch.empty(CALIB_BYTES // 2, dtype=torch.bfloat16, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"pmc_workload": "done", "kv_bytes": w.kv_bytes(), "calib_bytes": CALIB_BYTES}), flush=True)
+
+
+def summarize_pmc(fetch_dir: str, write_dir: str):
+    """Turn the FETCH_SIZE and WRITE_SIZE runs into the committed traffic summary."""
+    import csv
+    import glob
+
+    from paper_2609_08368_amd import workloads as wl
+
+    def per_kernel(d, counter):
+        # KiB per dispatch of the decode kernel, and of the calibration copies
+        # (the copy dispatches issued after the last decode dispatch)
+        rows = []
+        for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            rows += [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        per = {}
+        for r in rows:
+            key = (int(r["Dispatch_Id"]), r["Kernel_Name"])
+            per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+        dec = {k: v for k, v in per.items() if "decode_mfma_kernel" in k[1]}
+        last_dec = max(k[0] for k in dec)
+        cal = {k: v for k, v in per.items() if "copy" in k[1].lower() and k[0] > last_dec}
+        return {"decode": sum(dec.values()) / len(dec), "copy": sum(cal.values()) / len(cal)}
+
+    fetch = per_kernel(fetch_dir, "FETCH_SIZE")
+    write = per_kernel(write_dir, "WRITE_SIZE")
+    f_scale = CALIB_BYTES / (fetch["copy"] * 1024.0)
+    w_scale = CALIB_BYTES / (write["copy"] * 1024.0)
+    dec_fetch = fetch["decode"] * 1024.0 * f_scale
+    dec_write = write["decode"] * 1024.0 * w_scale
+    w = wl.decode_ragged()
+    res = {
+        "kernel": "decode_mfma_kernel", "workload": "ragged 64K decode batch (B128, Hq96/Hkv8, page 64)",
+        "source_hash": kernel_source_hash(),
+        "fetch_kib_per_dispatch": fetch["decode"], "write_kib_per_dispatch": write["decode"],
+        "copy_fetch_kib": fetch["copy"], "copy_write_kib": write["copy"], "calib_bytes": CALIB_BYTES,
+        "fetch_scale": f_scale, "write_scale": w_scale,
+        "hbm_read_bytes": dec_fetch, "hbm_write_bytes": dec_write, "traffic_bytes": dec_fetch + dec_write,
+        "algorithmic_bytes": w.kv_bytes(),
+        "traffic_over_algorithmic": (dec_fetch + dec_write) / w.kv_bytes(),
+    }
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(res, f, indent=1)
+    print(json.dumps(res, indent=1))
+
+
+def traffic_bytes():
+    """HBM bytes per decode launch from the committed counter summary, or None
+    when the summary is missing or the kernel sources changed since it was taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            d = json.load(f)
+    except (OSError, ValueError):
+        return None
+    return d["traffic_bytes"] if d.get("source_hash") == kernel_source_hash() else None
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -68,7 +163,16 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pmc-workload", action="store_true", help="run only what the counter runs profile")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write the HBM traffic summary from two rocprofv3 --pmc output directories")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc)
+        return
+    if args.pmc_workload:
+        pmc_workload()
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (the kernels run on one device's share; "
               "see DESIGN.md for how the work would shard). Run with --gpus 1.", file=sys.stderr)
@@ -200,7 +304,7 @@ def main():
         "roofline": {
             "kernel": "decode_mfma_kernel (ragged 64K decode batch)",
             "bound": "hbm", "achieved": round(kern_gbps, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-            "frac": round(kern_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+            "frac": round(kern_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic_bytes(),
             "kernel_ms": round(dec_kernel_ms, 4), "launches": n_k,
             "algorithmic_bytes": kv_dec,
         },
