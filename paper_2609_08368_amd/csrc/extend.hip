@@ -8,8 +8,8 @@
 // every row of a unit, so only the last steps of a unit apply the mask.
 //
 // The planner orders units longest key range first and keeps the units of one
-// (sequence, KV head) adjacent; the kernel maps workgroup ids so that adjacent
-// units run on the same XCD and share its L2 while they stream the same keys.
+// (sequence, KV head) adjacent, so they run at the same time and stream the
+// same keys through the L2s.
 #include "kernels.hpp"
 #include "tile_attn.hpp"
 
@@ -18,7 +18,6 @@ namespace rl {
 namespace {
 
 constexpr int kSortMax = 1024;          // sequences sorted by key count up to this batch size
-constexpr int kXcds = 8;
 
 struct SeqRange {
   int q0, n, kv;
@@ -100,15 +99,13 @@ __global__ __launch_bounds__(1024) void plan_extend_kernel(ExtendArgs a) {
 __global__ __launch_bounds__(256, 2) void extend_mfma_kernel(ExtendArgs a) {
   __shared__ TileLds lds;
 
-  // XCD-aware unit order: workgroup x runs on XCD x % 8; give each XCD a
-  // contiguous range of units so the units of one (sequence, KV head) share an L2.
-  const int total = a.ws.hdr[0];
-  const int per_xcd = (total + kXcds - 1) / kXcds;
-  const int x = blockIdx.x;
-  const int jx = x / kXcds;
-  if (jx >= per_xcd) return;
-  const int unit = (x % kXcds) * per_xcd + jx;
-  if (unit >= total) return;
+  // Units run in list order (longest key range first). Workgroups are handed
+  // to the XCDs round-robin, so each XCD gets every eighth unit: the work stays
+  // balanced across XCDs, and the units of one (sequence, KV head), which are
+  // adjacent in the list, run at the same time on every XCD, so each XCD's L2
+  // serves the shared keys to its share of them.
+  const int unit = blockIdx.x;
+  if (unit >= a.ws.hdr[0]) return;
   const int4 it = a.ws.items[unit];
   const int b = it.x, i0 = it.y, cnt = it.z, g = it.w & 0xffff, hb = it.w >> 16;
   int bad_seq = 0, bad = 0;               // sequence errors are reported by the planner
@@ -156,7 +153,7 @@ __global__ __launch_bounds__(256, 2) void extend_mfma_kernel(ExtendArgs a) {
 
 hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream, KernelTimer* timer) {
   plan_extend_kernel<<<1, 1024, 0, stream>>>(a);
-  const unsigned grid = (unsigned)((a.max_items + kXcds - 1) / kXcds * kXcds);
+  const unsigned grid = (unsigned)a.max_items;
   if (timer) (void)hipEventRecord(timer->start, stream);
   extend_mfma_kernel<<<grid, kTileWaves * 64, 0, stream>>>(a);
   if (timer) (void)hipEventRecord(timer->stop, stream);
