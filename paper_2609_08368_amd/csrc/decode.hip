@@ -474,7 +474,9 @@ __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
 // shared keys of a sub-group once for all its members' query rows (row r ->
 // member r / R, query head r % R), reading each shared page once, and writes
 // one partial per member into that member's slot for this split.
-__global__ __launch_bounds__(256, 2) void prefix_kernel(DecodeArgs a) {
+constexpr int kPrefixWaves = 4;         // waves per group-prefix workgroup: 128 member rows
+
+__global__ __launch_bounds__(kPrefixWaves * 64, 2) void prefix_kernel(DecodeArgs a) {
   __shared__ TileLds lds;
   // grid-stride over (shared item, KV head): a batch without trajectory groups
   // costs one small launch that exits at once
@@ -501,7 +503,7 @@ __global__ __launch_bounds__(256, 2) void prefix_kernel(DecodeArgs a) {
       for (int e = 0; e < 16; ++e) o[jd][e] = 0.f;
     float m_run = kNegInf, l_run = 0.f;
     int bad = 0;
-    tile_attend(a.kv, a.scale, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g, t0, t1, t1, t1 - 1, qv, lds, o, m_run,
+    tile_attend<kPrefixWaves>(a.kv, a.scale, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g, t0, t1, t1, t1 - 1, qv, lds, o, m_run,
                 l_run, bad);
     const HeadResult res = finish(m_run, l_run + __shfl_xor(l_run, 32, 64));
     if (row_ok) {
@@ -611,7 +613,7 @@ __global__ __launch_bounds__(64) void merge_kernel(MergeArgs a) {
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream, KernelTimer* timer) {
   plan_decode_kernel<<<1, 1024, 0, stream>>>(a);
   const unsigned per_item = a.R == 1 ? a.Hkv : a.Hkv * ((a.R + 15) / 16);
-  if (a.group_cap >= 2) prefix_kernel<<<(unsigned)a.prefix_grid, kTileWaves * 64, 0, stream>>>(a);
+  if (a.group_cap >= 2) prefix_kernel<<<(unsigned)a.prefix_grid, kPrefixWaves * 64, 0, stream>>>(a);
   if (timer) (void)hipEventRecord(timer->start, stream);
   if (a.R == 1) {
     decode_valu_kernel<<<(unsigned)a.max_items * per_item, 64, 0, stream>>>(a);

@@ -2,7 +2,7 @@
 // prefix plus, causally, to the chunk itself (bottom-right mask).
 //
 // A unit of work is (sequence b, KV head g, block of query heads, run of
-// chunk tokens): up to 128 query rows, token-major (row r -> token r / RB,
+// chunk tokens): up to 256 query rows, token-major (row r -> token r / RB,
 // head r % RB), all reading the same keys; one workgroup computes it with the
 // MFMA tile of tile_attn.hpp. Keys [0, prefix + first token) are visible to
 // every row of a unit, so only the last steps of a unit apply the mask.
@@ -96,7 +96,9 @@ __global__ __launch_bounds__(1024) void plan_extend_kernel(ExtendArgs a) {
   if (bad) atomicOr(a.ws.err, bad);
 }
 
-__global__ __launch_bounds__(256, 2) void extend_mfma_kernel(ExtendArgs a) {
+constexpr int kExtWaves = 8;            // waves per extend workgroup: 256 query rows per unit
+
+__global__ __launch_bounds__(kExtWaves * 64, 2) void extend_mfma_kernel(ExtendArgs a) {
   __shared__ TileLds lds;
 
   // Units run in list order (longest key range first). Workgroups are handed
@@ -132,7 +134,7 @@ __global__ __launch_bounds__(256, 2) void extend_mfma_kernel(ExtendArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[jd][e] = 0.f;
   float m_run = kNegInf, l_run = 0.f;
-  tile_attend(a.kv, a.scale, a.kv.bt + (int64_t)b * a.kv.bt_sb, g, 0, t_end, t_full, limit, qv, lds, o, m_run,
+  tile_attend<kExtWaves>(a.kv, a.scale, a.kv.bt + (int64_t)b * a.kv.bt_sb, g, 0, t_end, t_full, limit, qv, lds, o, m_run,
               l_run, bad);
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
@@ -155,7 +157,7 @@ hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream, KernelTimer* t
   plan_extend_kernel<<<1, 1024, 0, stream>>>(a);
   const unsigned grid = (unsigned)a.max_items;
   if (timer) (void)hipEventRecord(timer->start, stream);
-  extend_mfma_kernel<<<grid, kTileWaves * 64, 0, stream>>>(a);
+  extend_mfma_kernel<<<grid, kExtWaves * 64, 0, stream>>>(a);
   if (timer) (void)hipEventRecord(timer->stop, stream);
   return hipGetLastError();
 }

@@ -457,10 +457,13 @@ struct ExtendShape {
   int rows_head, tile_tokens, head_blocks;
 };
 
+// query rows per extend work unit: eight waves of 32 rows
+constexpr int kExtendRows = 256;
+
 ExtendShape extend_shape(int64_t R) {
   ExtendShape s;
-  s.rows_head = (int)std::min<int64_t>(R, 128);
-  s.tile_tokens = std::max(1, 128 / s.rows_head);
+  s.rows_head = (int)std::min<int64_t>(R, kExtendRows);
+  s.tile_tokens = std::max(1, kExtendRows / s.rows_head);
   s.head_blocks = (int)((R + s.rows_head - 1) / s.rows_head);
   return s;
 }

@@ -1,8 +1,8 @@
 // Multi-row attention tile on MFMA 32x32x16, shared by the extend kernel
 // (rows = chunk tokens x query heads) and the group-prefix kernel (rows =
-// trajectory-group members x query heads). A workgroup of four waves owns up
-// to 128 query rows that all read the same keys of one KV head; each wave owns
-// 32 rows, i.e. one 32-wide MFMA column block.
+// trajectory-group members x query heads). A workgroup of kWaves waves owns up
+// to 32 * kWaves query rows that all read the same keys of one KV head; each
+// wave owns 32 rows, i.e. one 32-wide MFMA column block.
 //
 // Per 64-key step the workgroup stages K and V of the step in LDS (double
 // buffered: the next step's rows are fetched into registers while the current
@@ -26,9 +26,7 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
-constexpr int kTileWaves = 4;              // waves per workgroup
 constexpr int kWaveRows = 32;              // query rows per wave
-constexpr int kTileRows = kTileWaves * kWaveRows;
 constexpr int kKeys = 64;                  // keys per step
 constexpr int kKStride = kHeadDim + 8;     // LDS row pitch of K (u16): 272 B
 constexpr int kVStride = kHeadDim + 32;    // LDS row pitch of V (u16): 320 B, spreads transpose loads over banks
@@ -57,6 +55,7 @@ __device__ __forceinline__ void load_q_operand(const __bf16* row, bool ok, bf16x
 // workgroup (no mask work for those steps). t_lo must be a multiple of kKeys.
 // Accumulates into o (O^T, 4 blocks of 32 dims), m_run (log2 units) and l_run
 // (this lane's half of the row sum; add lane ^ 32's for the total).
+template <int kWaves>
 __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, const int* bt_row, int g, int t_lo,
                                             int t_hi, int t_full, int limit, const bf16x8 (&qv)[8], TileLds& lds,
                                             f32x16 (&o)[4], float& m_run, float& l_run, int& bad) {
@@ -65,7 +64,9 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
   const int col = lane & 31, kg = lane >> 5;
   const float sl2 = scale * kLog2e;
 
-  // cooperative staging: thread -> (key rows tid/16 + 16 i, 16-byte chunk tid % 16)
+  // cooperative staging: thread -> (key rows tid/16 + kRowStep i, 16-byte chunk tid % 16)
+  constexpr int kRowStep = kWaves * 4;              // key rows covered by one pass of the workgroup
+  constexpr int kStageRows = kKeys / kRowStep;      // key rows each thread stages per step
   const uint32_t bt_sj = (uint32_t)kv.bt_sj;
   const int ld_row = tid >> 4, ld_chunk = (tid & 15) * 8;
   const __bf16* kbase = (const __bf16*)kv.k + (int64_t)g * kv.sh + ld_chunk;
@@ -77,20 +78,20 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
   // per step. Page ids are loaded one step ahead of the K/V rows they address,
   // so a step's row loads never wait for a block-table load.
   const bool page_holds_step = kv.page_size >= kKeys;
-  bf16x8 kr[4], vr[4];
-  int praw[4];
+  bf16x8 kr[kStageRows], vr[kStageRows];
+  int praw[kStageRows];
   auto fetch_pages = [&](int t0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int t = t0 + (page_holds_step ? 0 : ld_row + 16 * i);
+    for (int i = 0; i < kStageRows; ++i) {
+      int t = t0 + (page_holds_step ? 0 : ld_row + kRowStep * i);
       t = t < t_hi ? t : t_hi - 1;
       praw[i] = (page_holds_step && i) ? 0 : bt_row[__umul24((uint32_t)(t >> kv.log2_page), bt_sj)];
     }
   };
   auto fetch_rows = [&](int t0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int t = t0 + ld_row + 16 * i;
+    for (int i = 0; i < kStageRows; ++i) {
+      int t = t0 + ld_row + kRowStep * i;
       t = t < t_hi ? t : t_hi - 1;
       int pg = praw[page_holds_step ? 0 : i];
       if ((unsigned)pg >= (unsigned)kv.num_pages) {
@@ -103,9 +104,9 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
   };
   auto stage = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      *reinterpret_cast<bf16x8*>(&lds.ks[buf][ld_row + 16 * i][ld_chunk]) = kr[i];
-      *reinterpret_cast<bf16x8*>(&lds.vs[buf][ld_row + 16 * i][ld_chunk]) = vr[i];
+    for (int i = 0; i < kStageRows; ++i) {
+      *reinterpret_cast<bf16x8*>(&lds.ks[buf][ld_row + kRowStep * i][ld_chunk]) = kr[i];
+      *reinterpret_cast<bf16x8*>(&lds.vs[buf][ld_row + kRowStep * i][ld_chunk]) = vr[i];
     }
   };
 
