@@ -503,7 +503,7 @@ __global__ __launch_bounds__(kPrefixWaves * 64, 2) void prefix_kernel(DecodeArgs
       for (int e = 0; e < 16; ++e) o[jd][e] = 0.f;
     float m_run = kNegInf, l_run = 0.f;
     int bad = 0;
-    tile_attend<kPrefixWaves>(a.kv, a.scale, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g, t0, t1, t1, t1 - 1, qv, lds, o, m_run,
+    tile_attend<kPrefixWaves, false>(a.kv, a.scale, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g, t0, t1, t1, t1 - 1, qv, lds, o, m_run,
                 l_run, bad);
     const HeadResult res = finish(m_run, l_run + __shfl_xor(l_run, 32, 64));
     if (row_ok) {

@@ -5,8 +5,9 @@
 // wave owns 32 rows, i.e. one 32-wide MFMA column block.
 //
 // Per 64-key step the workgroup stages K and V of the step in LDS (double
-// buffered: the next step's rows are fetched into registers while the current
-// step computes, and page ids one step before that), then every wave computes
+// buffered: the rows of a later step are fetched into registers while the
+// current step computes -- one step ahead, or two with kDeep -- and page ids
+// one step before the rows they address), then every wave computes
 //   S^T = K Q^T            (A = K rows from LDS, B = Q held in registers),
 //   P^T = exp2(S^T - m)    (per query column, in registers),
 //   O^T += V^T P^T         (A = V^T read with the LDS transpose load),
@@ -55,7 +56,7 @@ __device__ __forceinline__ void load_q_operand(const __bf16* row, bool ok, bf16x
 // workgroup (no mask work for those steps). t_lo must be a multiple of kKeys.
 // Accumulates into o (O^T, 4 blocks of 32 dims), m_run (log2 units) and l_run
 // (this lane's half of the row sum; add lane ^ 32's for the total).
-template <int kWaves>
+template <int kWaves, bool kDeep>
 __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, const int* bt_row, int g, int t_lo,
                                             int t_hi, int t_full, int limit, const bf16x8 (&qv)[8], TileLds& lds,
                                             f32x16 (&o)[4], float& m_run, float& l_run, int& bad) {
@@ -78,7 +79,6 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
   // per step. Page ids are loaded one step ahead of the K/V rows they address,
   // so a step's row loads never wait for a block-table load.
   const bool page_holds_step = kv.page_size >= kKeys;
-  bf16x8 kr[kStageRows], vr[kStageRows];
   int praw[kStageRows];
   auto fetch_pages = [&](int t0) {
 #pragma unroll
@@ -88,7 +88,8 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
       praw[i] = (page_holds_step && i) ? 0 : bt_row[__umul24((uint32_t)(t >> kv.log2_page), bt_sj)];
     }
   };
-  auto fetch_rows = [&](int t0) {
+  typedef bf16x8 Rows[kStageRows];
+  auto fetch_rows = [&](int t0, Rows& kr, Rows& vr) {
 #pragma unroll
     for (int i = 0; i < kStageRows; ++i) {
       int t = t0 + ld_row + kRowStep * i;
@@ -102,7 +103,7 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
       vr[i] = load_bf16x8(vbase + row_offset((uint32_t)pg, vsp, t & pmask, vss));
     }
   };
-  auto stage = [&](int buf) {
+  auto stage = [&](int buf, const Rows& kr, const Rows& vr) {
 #pragma unroll
     for (int i = 0; i < kStageRows; ++i) {
       *reinterpret_cast<bf16x8*>(&lds.ks[buf][ld_row + kRowStep * i][ld_chunk]) = kr[i];
@@ -120,32 +121,38 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
   if (t_lo >= t_hi) return;
-  fetch_pages(t_lo);
-  fetch_rows(t_lo);
-  stage(0);
-  if (t_lo + kKeys < t_hi) fetch_pages(t_lo + kKeys);
-  __syncthreads();
-  int buf = 0;
-  for (int t0 = t_lo; t0 < t_hi; t0 += kKeys) {
-    const bool more = t0 + kKeys < t_hi;
-    if (more) {
-      fetch_rows(t0 + kKeys);
-      if (t0 + 2 * kKeys < t_hi) fetch_pages(t0 + 2 * kKeys);
+  const int nsteps = (t_hi - t_lo + kKeys - 1) / kKeys;
+
+  // one step: prefetch, S^T, softmax, PV, then stage the next step's rows
+  auto step = [&](int j, Rows& k_next, Rows& v_next, Rows& k_free, Rows& v_free) {
+    const int t0 = t_lo + j * kKeys;
+    const int buf = j & 1;
+    if constexpr (kDeep) {
+      // rows of step j+2 go into the set staged at the end of step j-1
+      if (j + 2 < nsteps) {
+        fetch_rows(t0 + 2 * kKeys, k_free, v_free);
+        if (j + 3 < nsteps) fetch_pages(t0 + 3 * kKeys);
+      }
+    } else {
+      if (j + 1 < nsteps) {
+        fetch_rows(t0 + kKeys, k_next, v_next);
+        if (j + 2 < nsteps) fetch_pages(t0 + 2 * kKeys);
+      }
     }
 
     // S^T for the two 32-key blocks of this step; the two accumulation chains
     // are interleaved so each MFMA's predecessor in its chain has retired
-    f32x16 s[2];
+    f32x16 sc[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) s[kb][e] = 0.f;
+      for (int e = 0; e < 16; ++e) sc[kb][e] = 0.f;
 #pragma unroll
     for (int c = 0; c < 8; ++c)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         const bf16x8 kop = *reinterpret_cast<const bf16x8*>(&lds.ks[buf][32 * kb + col][16 * c + 8 * kg]);
-        s[kb] = mfma_32x32x16(kop, qv[c], s[kb]);
+        sc[kb] = mfma_32x32x16(kop, qv[c], sc[kb]);
       }
 
     // Row max of the raw scores (the positive scale commutes with max and is
@@ -158,13 +165,13 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int key = t0 + 32 * kb + 8 * (e >> 2) + 4 * kg + (e & 3);
-          if (key > limit || key >= t_hi) s[kb][e] = kNegInf;
+          if (key > limit || key >= t_hi) sc[kb][e] = kNegInf;
         }
     }
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int e = 0; e < 16; e += 2) mt = fmaxf(mt, fmaxf(s[kb][e], s[kb][e + 1]));
+      for (int e = 0; e < 16; e += 2) mt = fmaxf(mt, fmaxf(sc[kb][e], sc[kb][e + 1]));
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * sl2;
     // lazy rescale: raise the running max only when the step's max exceeds it by 2^8
     const bool raise = mt > m_run + kLazy;
@@ -186,7 +193,7 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
     for (int h = 0; h < 4; ++h)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float p = exp2_fast(fmaf(s[h >> 1][8 * (h & 1) + e], sl2, neg_m));
+        const float p = exp2_fast(fmaf(sc[h >> 1][8 * (h & 1) + e], sl2, neg_m));
         ps[e & 3] += p;
         pb[h][e] = (__bf16)p;
       }
@@ -204,11 +211,31 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
         o[jd] = mfma_32x32x16(__builtin_bit_cast(bf16x8, v8), pb[h], o[jd]);
       }
     }
-    if (more) {
-      stage(buf ^ 1);
+    if (j + 1 < nsteps) {
+      stage(buf ^ 1, k_next, v_next);
       __syncthreads();
-      buf ^= 1;
     }
+  };
+
+  Rows ka, va, kb2, vb2;
+  fetch_pages(t_lo);
+  fetch_rows(t_lo, ka, va);
+  stage(0, ka, va);
+  if (nsteps > 1) fetch_pages(t_lo + kKeys);
+  if constexpr (kDeep) {
+    // two steps in flight: rows of step 1 load now, page ids of step 2 too
+    if (nsteps > 1) {
+      fetch_rows(t_lo + kKeys, kb2, vb2);
+      if (nsteps > 2) fetch_pages(t_lo + 2 * kKeys);
+    }
+    __syncthreads();
+    for (int j = 0; j < nsteps; j += 2) {
+      step(j, kb2, vb2, ka, va);
+      if (j + 1 < nsteps) step(j + 1, ka, va, kb2, vb2);
+    }
+  } else {
+    __syncthreads();
+    for (int j = 0; j < nsteps; ++j) step(j, ka, va, ka, va);
   }
 }
 
