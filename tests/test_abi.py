@@ -146,3 +146,12 @@ def test_merge_validation():
 def test_valid_call_without_gpu_reports_hip_error():
     rc = call_decode(decode_args())
     assert ra.STATUS[rc] in ("RL_ERR_HIP", "RL_ERR_WORKSPACE"), ra.last_error()
+
+
+@pytest.mark.parametrize("scale", [float("nan"), 0.0, -0.1, float("inf")])
+def test_scale_must_be_positive_and_finite(scale):
+    a = decode_args()
+    r = ctypes.byref
+    rc = ra.lib().rl_attn_decode_ex(r(a["q"]), r(a["k"]), r(a["v"]), r(a["bt"]), r(a["lens"]), ctypes.c_float(scale),
+                                    r(a["out"]), None, None, None)
+    assert ra.STATUS[rc] == "RL_ERR_INVALID_ARG" and "scale" in ra.last_error()
