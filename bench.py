@@ -66,15 +66,16 @@ CALIB_BYTES = 2 << 30   # bytes read and bytes written by the calibration copy
 
 
 def kernel_source_hash() -> str:
-    """Hash of the HIP sources the decode kernel is built from."""
+    """Hash of the HIP sources and build flags the decode kernel is built from."""
     import hashlib
 
     h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2609_08368_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".hpp", ".cpp")):
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(name.encode() + f.read())
+    pkg = os.path.join(ROOT, "paper_2609_08368_amd")
+    csrc = os.path.join(pkg, "csrc")
+    files = [os.path.join(csrc, n) for n in sorted(os.listdir(csrc)) if n.endswith((".hip", ".hpp", ".cpp"))]
+    for path in files + [os.path.join(pkg, "build.py")]:
+        with open(path, "rb") as f:
+            h.update(os.path.basename(path).encode() + f.read())
     return h.hexdigest()[:16]
 
 

@@ -16,7 +16,8 @@ from typing import Optional
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "librlattn.so")
+# RL_ATTN_LIB selects another build of the library (A/B comparisons of builds)
+LIB_PATH = os.environ.get("RL_ATTN_LIB", os.path.join(_PKG, "librlattn.so"))
 HEADER = os.path.join(os.path.dirname(_PKG), "include", "rl_attn.h")
 
 RL_BF16, RL_F32, RL_I32 = 1, 2, 3
