@@ -38,12 +38,57 @@ __device__ __forceinline__ f32x4 mfma_16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
-__device__ __forceinline__ float xor_max(float v, int mask) { return fmaxf(v, __shfl_xor(v, mask, 64)); }
-__device__ __forceinline__ float xor_sum(float v, int mask) { return v + __shfl_xor(v, mask, 64); }
+// Cross-lane exchanges that stay in the VALU (no LDS round trip). Inside a
+// 16-lane row DPP permutes operands: quad_perm [1,0,3,2] and [2,3,0,1] pair
+// lane l with l^1 and l^2, half_mirror pairs l with 7-l inside 8 lanes and
+// mirror pairs l with 15-l. Across rows and halves, the gfx950 lane swaps
+// exchange rows 2i and 2i+1 (permlane16) or lanes l and l+32 (permlane32);
+// each returns both swapped registers, and as the two hold, in every lane, the
+// lane's own value and its partner's, their max or sum is the pair's.
+template <int kCtrl>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), kCtrl, 0xf, 0xf, false));
+}
+constexpr int kDppXor1 = 0xb1;         // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4e;         // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;  // l -> 7 - l within 8 lanes
+constexpr int kDppMirror = 0x140;      // l -> 15 - l within 16 lanes
 
+__device__ __forceinline__ float max_l16(float v) {   // max over lanes l, l^16
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_l16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float max_l32(float v) {   // max over lanes l, l^32
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_l32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+// Sum over the 16 lanes of a row; every lane of the row receives it.
+__device__ __forceinline__ float row_sum16(float v) {
+  v += dpp<kDppXor1>(v);
+  v += dpp<kDppXor2>(v);
+  v += dpp<kDppHalfMirror>(v);
+  return v + dpp<kDppMirror>(v);
+}
 // Max / sum over the four lane groups (lanes l, l^16, l^32, l^48).
-__device__ __forceinline__ float group_max(float v) { return xor_max(xor_max(v, 16), 32); }
-__device__ __forceinline__ float group_sum(float v) { return xor_sum(xor_sum(v, 16), 32); }
+__device__ __forceinline__ float group_max(float v) { return max_l32(max_l16(v)); }
+__device__ __forceinline__ float group_sum(float v) { return sum_l32(sum_l16(v)); }
+// Max / sum over all 64 lanes; every lane receives it.
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, dpp<kDppXor1>(v));
+  v = fmaxf(v, dpp<kDppXor2>(v));
+  v = fmaxf(v, dpp<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp<kDppMirror>(v));
+  return group_max(v);
+}
+__device__ __forceinline__ float wave_sum(float v) { return group_sum(row_sum16(v)); }
 
 __device__ __forceinline__ bf16x8 zero_bf16x8() {
   bf16x8 z;

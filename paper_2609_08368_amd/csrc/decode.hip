@@ -427,10 +427,7 @@ __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
     float d = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) d += qf[i] * (float)kk[i];
-    d = xor_sum(d, 1);
-    d = xor_sum(d, 2);
-    d = xor_sum(d, 4);
-    d = xor_sum(d, 8);
+    d = row_sum16(d);
     if (valid) {
       const float m_new = fmaxf(m, d);
       const float alpha = exp2_fast(m - m_new);
@@ -505,7 +502,7 @@ __global__ __launch_bounds__(kPrefixWaves * 64, 2) void prefix_kernel(DecodeArgs
     int bad = 0;
     tile_attend<kPrefixWaves, false>(a.kv, a.scale, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g, t0, t1, t1, t1 - 1, qv, lds, o, m_run,
                 l_run, bad);
-    const HeadResult res = finish(m_run, l_run + __shfl_xor(l_run, 32, 64));
+    const HeadResult res = finish(m_run, sum_l32(l_run));
     if (row_ok) {
       const int slot = a.ws.base[b] + split;
       if (slot < a.max_slots) {
@@ -528,8 +525,7 @@ __device__ __forceinline__ void merge_parts(const float* o_base, int64_t o_step,
   float M = kNegInf;
   for (int s0 = 0; s0 < n; s0 += 64)
     if (s0 + lane < n) M = fmaxf(M, l_base[(int64_t)(s0 + lane) * l_step]);
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
+  M = wave_max(M);
   float z = 0.f, a0 = 0.f, a1 = 0.f;
   if (M != kNegInf) {
     for (int s0 = 0; s0 < n; s0 += 64) {
@@ -556,8 +552,7 @@ __device__ __forceinline__ void merge_parts(const float* o_base, int64_t o_step,
         a1 += w * v.y;
       }
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) z += __shfl_xor(z, o, 64);
+    z = wave_sum(z);
   }
   const float inv = z > 0.f ? 1.f / z : 0.f;
   out2[0] = a0 * inv;

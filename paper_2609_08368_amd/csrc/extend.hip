@@ -134,10 +134,13 @@ __global__ __launch_bounds__(kExtWaves * 64, 2) void extend_mfma_kernel(ExtendAr
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[jd][e] = 0.f;
   float m_run = kNegInf, l_run = 0.f;
-  tile_attend<kExtWaves, true>(a.kv, a.scale, a.kv.bt + (int64_t)b * a.kv.bt_sb, g, 0, t_end, t_full, limit, qv, lds, o, m_run,
-              l_run, bad);
+  const int* bt_row = a.kv.bt + (int64_t)b * a.kv.bt_sb;
+  if (uniform_pages(a.kv))
+    tile_attend_pp<kExtWaves, true>(a.kv, a.scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run, l_run, bad);
+  else
+    tile_attend_pp<kExtWaves, false>(a.kv, a.scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run, l_run, bad);
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float l_tot = sum_l32(l_run);
   if (row_ok) {
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
     if (a.out_f32)

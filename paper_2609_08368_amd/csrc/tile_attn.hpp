@@ -18,6 +18,8 @@
 // O^T rescale (64 multiplies per lane) is skipped on almost every step.
 #pragma once
 
+#include <type_traits>
+
 #include "attn_common.hpp"
 
 namespace rl {
@@ -37,6 +39,13 @@ struct TileLds {
   u16 ks[2][kKeys][kKStride];
   u16 vs[2][kKeys][kVStride];
 };
+
+// A page holds whole 64-key steps and every in-page byte offset of K and V fits
+// 31 bits (the condition of the scalar page-lookup fetch below).
+__device__ __forceinline__ bool uniform_pages(const PagedKV& kv) {
+  const int64_t ss = kv.ss > kv.v_ss ? kv.ss : kv.v_ss;
+  return kv.page_size >= kKeys && ((int64_t)kv.page_size * ss + kHeadDim) * 2 < (int64_t(1) << 31);
+}
 
 __device__ __forceinline__ f32x16 mfma_32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -142,18 +151,30 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
 
     // S^T for the two 32-key blocks of this step; the two accumulation chains
     // are interleaved so each MFMA's predecessor in its chain has retired
+    // K operands are read two 16-dimension slices ahead of their MFMAs; the
+    // scheduling fences keep the compiler from moving each read next to its
+    // use, which would leave one LDS read in flight per wave
     f32x16 sc[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) sc[kb][e] = 0.f;
+    bf16x8 kop[3][2];
+    auto read_k = [&](int c, bf16x8 (&dst)[2]) {
 #pragma unroll
-    for (int c = 0; c < 8; ++c)
+      for (int kb = 0; kb < 2; ++kb)
+        dst[kb] = *reinterpret_cast<const bf16x8*>(&lds.ks[buf][32 * kb + col][16 * c + 8 * kg]);
+    };
+    read_k(0, kop[0]);
+    read_k(1, kop[1]);
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const bf16x8 kop = *reinterpret_cast<const bf16x8*>(&lds.ks[buf][32 * kb + col][16 * c + 8 * kg]);
-        sc[kb] = mfma_32x32x16(kop, qv[c], sc[kb]);
-      }
+    for (int c = 0; c < 8; ++c) {
+      if (c + 2 < 8) read_k(c + 2, kop[(c + 2) % 3]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) sc[kb] = mfma_32x32x16(kop[c % 3][kb], qv[c], sc[kb]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
 
     // Row max of the raw scores (the positive scale commutes with max and is
     // folded into the exponent below); the mask only where some column cannot
@@ -172,7 +193,7 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int e = 0; e < 16; e += 2) mt = fmaxf(mt, fmaxf(sc[kb][e], sc[kb][e + 1]));
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64)) * sl2;
+    mt = max_l32(mt) * sl2;
     // lazy rescale: raise the running max only when the step's max exceeds it by 2^8
     const bool raise = mt > m_run + kLazy;
     if (__builtin_amdgcn_ballot_w64(raise) != 0) {
@@ -237,6 +258,274 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
     __syncthreads();
     for (int j = 0; j < nsteps; ++j) step(j, ka, va, ka, va);
   }
+}
+
+// The same attention with a ping-pong schedule for eight waves (two per SIMD).
+// Waves 0-3 and 4-7 form two groups that each hold one wave of every SIMD. A
+// step is split into an MFMA phase (O^T += V^T P^T of the previous step, then
+// S^T of this step) and a softmax phase, separated by workgroup barriers; the
+// second group starts one barrier late, so on every SIMD one wave issues MFMAs
+// while the other runs the softmax, and they swap at every barrier.
+// K is staged one step ahead of V: in its MFMA phase of step j each wave writes
+// its rows of K(j+1) and V(j), which are read only after the barrier that ends
+// the second group's MFMA phase of step j; the buffers they overwrite (K(j-1),
+// V(j-2)) were last read before the barrier that ended that group's MFMA phase
+// of step j-1, and every write happens after it. Both groups pass the same
+// number of barriers. The LDS buffers are still being read when the first
+// group returns: a caller that reuses them must synchronise the workgroup.
+//
+// kUniformPages: a page holds whole steps (page size >= kKeys) and in-page
+// byte offsets fit 31 bits. A step's page id is then the same for the whole
+// workgroup: it is read with a scalar load (through the constant address
+// space; the block table is not written while the kernel runs), the page base
+// is formed on the scalar unit, and a thread's in-page row offsets are fixed
+// except for the clamp to the last key in the sequence's final step.
+// Otherwise every thread looks up the page of each row it stages.
+template <int kWaves, bool kUniformPages>
+__device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, const int* bt_row, int g, int t_lo,
+                                               int t_hi, int t_full, int limit, const bf16x8 (&qv)[8], TileLds& lds,
+                                               f32x16 (&o)[4], float& m_run, float& l_run, int& bad) {
+  static_assert(kWaves == 8, "the ping-pong schedule pairs two waves on each SIMD");
+  constexpr int kAhead = 3;                       // LDS operand reads in flight ahead of the MFMAs
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int col = lane & 31, kg = lane >> 5;
+  const bool late = (tid >> 6) >= 4;
+  const float sl2 = scale * kLog2e;
+
+  constexpr int kRowStep = kWaves * 4;
+  constexpr int kStageRows = kKeys / kRowStep;
+  typedef bf16x8 Rows[kStageRows];
+  const uint32_t bt_sj = (uint32_t)kv.bt_sj;
+  const int ld_row = tid >> 4, ld_chunk = (tid & 15) * 8;
+  const int pmask = kv.page_size - 1;
+  auto put_k = [&](int buf, const Rows& r) {
+#pragma unroll
+    for (int i = 0; i < kStageRows; ++i)
+      *reinterpret_cast<bf16x8*>(&lds.ks[buf][ld_row + kRowStep * i][ld_chunk]) = r[i];
+  };
+  auto put_v = [&](int buf, const Rows& r) {
+#pragma unroll
+    for (int i = 0; i < kStageRows; ++i)
+      *reinterpret_cast<bf16x8*>(&lds.vs[buf][ld_row + kRowStep * i][ld_chunk]) = r[i];
+  };
+  const int tr_row = 4 * kg + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+
+  if (t_lo >= t_hi) return;
+  const int nsteps = (t_hi - t_lo + kKeys - 1) / kKeys;
+  const int t_last = t_lo + (nsteps - 1) * kKeys;     // first key of the final step
+
+  // ---- row fetch, per-row page lookups --------------------------------------
+  typedef int Ids[kStageRows];
+  const __bf16* kbase = (const __bf16*)kv.k + (int64_t)g * kv.sh + ld_chunk;
+  const __bf16* vbase = (const __bf16*)kv.v + (int64_t)g * kv.v_sh + ld_chunk;
+  const uint32_t ksp = (uint32_t)kv.sp, kss = (uint32_t)kv.ss;
+  const uint32_t vsp = (uint32_t)kv.v_sp, vss = (uint32_t)kv.v_ss;
+  const bool page_holds_step = kv.page_size >= kKeys;
+  auto load_ids = [&](int t0, Ids& ids) {
+#pragma unroll
+    for (int i = 0; i < kStageRows; ++i) {
+      int t = t0 + (page_holds_step ? 0 : ld_row + kRowStep * i);
+      t = t < t_hi ? t : t_hi - 1;
+      ids[i] = (page_holds_step && i) ? 0 : bt_row[__umul24((uint32_t)(t >> kv.log2_page), bt_sj)];
+    }
+  };
+  auto fetch = [&](int t0, const Ids& ids, const __bf16* base, uint32_t sp, uint32_t ss, Rows& r) {
+#pragma unroll
+    for (int i = 0; i < kStageRows; ++i) {
+      int t = t0 + ld_row + kRowStep * i;
+      t = t < t_hi ? t : t_hi - 1;
+      int pg = ids[page_holds_step ? 0 : i];
+      if ((unsigned)pg >= (unsigned)kv.num_pages) {
+        bad = 1;
+        pg = pg < 0 ? 0 : kv.num_pages - 1;
+      }
+      r[i] = load_bf16x8(base + row_offset((uint32_t)pg, sp, t & pmask, ss));
+    }
+  };
+
+  // ---- row fetch, one scalar page lookup per step ----------------------------
+  typedef __attribute__((address_space(4))) const int ConstInt;
+  const ConstInt* bt_c = (const ConstInt*)bt_row;
+  const char* kbase_u = (const char*)((const __bf16*)kv.k + (int64_t)g * kv.sh);
+  const char* vbase_u = (const char*)((const __bf16*)kv.v + (int64_t)g * kv.v_sh);
+  uint32_t koff[kStageRows], voff[kStageRows];        // byte offsets of this thread's rows in a step
+#pragma unroll
+  for (int i = 0; i < kStageRows; ++i) {
+    koff[i] = 2u * (ld_chunk + (uint32_t)(ld_row + kRowStep * i) * kss);
+    voff[i] = 2u * (ld_chunk + (uint32_t)(ld_row + kRowStep * i) * vss);
+  }
+  auto page_id = [&](int t0) -> int {
+    const int t = t0 < t_last ? t0 : t_last;
+    int pg = bt_c[__umul24((uint32_t)(t >> kv.log2_page), bt_sj)];
+    if ((unsigned)pg >= (unsigned)kv.num_pages) {
+      bad = 1;
+      pg = pg < 0 ? 0 : kv.num_pages - 1;
+    }
+    return pg;
+  };
+  auto fetch_u = [&](int t0, int pg, const char* base, int64_t sp, uint32_t ss, const uint32_t (&off)[kStageRows],
+                     Rows& r) {
+    const int tc = t0 < t_last ? t0 : t_last;
+    const char* pb = base + 2 * ((int64_t)pg * sp) + 2u * ((uint32_t)(tc & pmask) * ss);
+    if (tc + kKeys <= t_hi) {
+#pragma unroll
+      for (int i = 0; i < kStageRows; ++i) r[i] = *reinterpret_cast<const bf16x8*>(pb + off[i]);
+    } else {
+      const int last = t_hi - 1 - tc;
+#pragma unroll
+      for (int i = 0; i < kStageRows; ++i) {
+        const int rr = min(ld_row + kRowStep * i, last);
+        r[i] = *reinterpret_cast<const bf16x8*>(pb + 2u * (ld_chunk + (uint32_t)rr * ss));
+      }
+    }
+  };
+
+  f32x16 sc[2];
+  bf16x8 pb[4];
+
+  // MFMA phase: operands are read kAhead MFMAs ahead; the fences keep each
+  // read ahead of the MFMAs that do not need it
+  auto mfma_phase = [&](auto pv_tag, auto s_tag, int vbuf, int kbuf) {
+    constexpr bool kPV = decltype(pv_tag)::value, kS = decltype(s_tag)::value;
+    constexpr int i0 = kPV ? 0 : 16, i1 = kS ? 32 : 16;
+    if constexpr (kS) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sc[kb][e] = 0.f;
+    }
+    auto read = [&](int i) -> bf16x8 {
+      if (i < 16) {
+        const u16* vp = &lds.vs[vbuf][16 * (i >> 2) + tr_row][32 * (i & 3) + tr_col];
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)vp);
+        const i16x4 up = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vp + 8 * kVStride));
+        return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+      const int c = (i - 16) >> 1, kb = (i - 16) & 1;
+      return *reinterpret_cast<const bf16x8*>(&lds.ks[kbuf][32 * kb + col][16 * c + 8 * kg]);
+    };
+    bf16x8 ring[kAhead + 1];
+#pragma unroll
+    for (int i = i0; i < i0 + kAhead; ++i) ring[i % (kAhead + 1)] = read(i);
+#pragma unroll
+    for (int i = i0; i < i1; ++i) {
+      if (i + kAhead < i1) ring[(i + kAhead) % (kAhead + 1)] = read(i + kAhead);
+      __builtin_amdgcn_sched_barrier(0);
+      if (i < 16)
+        o[i & 3] = mfma_32x32x16(ring[i % (kAhead + 1)], pb[i >> 2], o[i & 3]);
+      else
+        sc[(i - 16) & 1] = mfma_32x32x16(ring[i % (kAhead + 1)], qv[(i - 16) >> 1], sc[(i - 16) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // softmax phase of the step starting at key t0: S^T -> P^T (bf16), running max and sum
+  auto softmax_phase = [&](int t0) {
+    float mt = kNegInf;
+    if (t0 + kKeys > t_full) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = t0 + 32 * kb + 8 * (e >> 2) + 4 * kg + (e & 3);
+          if (key > limit || key >= t_hi) sc[kb][e] = kNegInf;
+        }
+    }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; e += 2) mt = fmaxf(mt, fmaxf(sc[kb][e], sc[kb][e + 1]));
+    mt = max_l32(mt) * sl2;
+    const bool raise = mt > m_run + kLazy;
+    if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+      const float m_new = raise ? mt : m_run;
+      const float alpha = exp2_fast(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int jd = 0; jd < 4; ++jd) o[jd] *= alpha;
+      m_run = m_new;
+    }
+    const float neg_m = -m_run;
+    float ps[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int h = 0; h < 4; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float p = exp2_fast(fmaf(sc[h >> 1][8 * (h & 1) + e], sl2, neg_m));
+        ps[e & 3] += p;
+        pb[h][e] = (__bf16)p;
+      }
+    l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
+  };
+
+  // Row fetches past the final step read that step again: the loads stay
+  // unconditional, so no register copy has to wait for them.
+  // Invariant at the top of step j: kr = rows of K(j+1), vr = rows of V(j);
+  // ids (or scalar page ids) of steps j+1 and j+2 are at hand.
+  Rows kr, vr;
+  Ids id_k, id_v;
+  int pid_1 = 0, pid_2 = 0;
+  if constexpr (kUniformPages) {
+    const int p0 = page_id(t_lo);
+    fetch_u(t_lo, p0, kbase_u, kv.sp, kss, koff, kr);
+    fetch_u(t_lo, p0, vbase_u, kv.v_sp, vss, voff, vr);
+    put_k(0, kr);
+    pid_1 = page_id(t_lo + kKeys);
+    fetch_u(t_lo + kKeys, pid_1, kbase_u, kv.sp, kss, koff, kr);
+    pid_2 = page_id(t_lo + 2 * kKeys);
+  } else {
+    load_ids(t_lo, id_k);
+    fetch(t_lo, id_k, kbase, ksp, kss, kr);
+    fetch(t_lo, id_k, vbase, vsp, vss, vr);
+    put_k(0, kr);
+    load_ids(t_lo + kKeys, id_v);
+    fetch(t_lo + kKeys, id_v, kbase, ksp, kss, kr);
+    load_ids(t_lo + 2 * kKeys, id_k);
+  }
+  __syncthreads();
+  if (late) __syncthreads();
+
+  auto stage_and_fetch = [&](int j) {
+    const int t0 = t_lo + j * kKeys;
+    if (j + 1 < nsteps) put_k((j + 1) & 1, kr);
+    put_v(j & 1, vr);
+    if constexpr (kUniformPages) {
+      fetch_u(t0 + kKeys, pid_1, vbase_u, kv.v_sp, vss, voff, vr);
+      fetch_u(t0 + 2 * kKeys, pid_2, kbase_u, kv.sp, kss, koff, kr);
+      pid_1 = pid_2;
+    } else {
+      fetch(t0 + kKeys, id_v, vbase, vsp, vss, vr);
+      fetch(t0 + 2 * kKeys, id_k, kbase, ksp, kss, kr);
+#pragma unroll
+      for (int i = 0; i < kStageRows; ++i) id_v[i] = id_k[i];
+      load_ids(t0 + 3 * kKeys, id_k);
+    }
+  };
+  // the scalar page id of step j+3 is read at the end of step j's softmax
+  // phase, so the barrier's wait covers its latency
+  auto next_page = [&](int j) {
+    if constexpr (kUniformPages) pid_2 = page_id(t_lo + (j + 3) * kKeys);
+  };
+  const std::true_type yes{};
+  const std::false_type no{};
+  stage_and_fetch(0);
+  mfma_phase(no, yes, 0, 0);
+  __syncthreads();
+  softmax_phase(t_lo);
+  next_page(0);
+  __syncthreads();
+  for (int j = 1; j < nsteps; ++j) {
+    stage_and_fetch(j);
+    mfma_phase(yes, yes, (j - 1) & 1, j & 1);
+    __syncthreads();
+    softmax_phase(t_lo + j * kKeys);
+    next_page(j);
+    __syncthreads();
+  }
+  mfma_phase(yes, no, (nsteps - 1) & 1, 0);
+  if (!late) __syncthreads();
 }
 
 // Normalised output row of this lane's column: element (jd, q, i) of o holds
