@@ -510,15 +510,18 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
   };
   const std::true_type yes{};
   const std::false_type no{};
-  stage_and_fetch(0);
+  // the staging of a step follows its MFMAs: they start as soon as the
+  // barrier opens, and the rows fetched one step earlier get the MFMA phase's
+  // time to arrive
   mfma_phase(no, yes, 0, 0);
+  stage_and_fetch(0);
   __syncthreads();
   softmax_phase(t_lo);
   next_page(0);
   __syncthreads();
   for (int j = 1; j < nsteps; ++j) {
-    stage_and_fetch(j);
     mfma_phase(yes, yes, (j - 1) & 1, j & 1);
+    stage_and_fetch(j);
     __syncthreads();
     softmax_phase(t_lo + j * kKeys);
     next_page(j);
