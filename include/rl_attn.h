@@ -84,8 +84,10 @@ enum rl_prefix_mode { RL_PREFIX_AUTO = 0, RL_PREFIX_OFF = 1 };
 
 /* Options for the _ex calls. A NULL pointer means all defaults (zeros). */
 typedef struct {
-  int32_t split_tokens;  /* decode: tokens per split-KV partial; 0 = automatic,
-                            otherwise a multiple of 64 (RL_ERR_INVALID_ARG if not) */
+  int32_t split_tokens;  /* decode: keys per split-KV partial (private keys: per
+                            worker share; group-shared keys: per shared split);
+                            0 = automatic, otherwise a multiple of 64
+                            (RL_ERR_INVALID_ARG if not)                          */
   int32_t prefix_share;  /* enum rl_prefix_mode: read group-shared prefix pages once
                             (AUTO) or treat every sequence independently (OFF)     */
   int32_t validate;      /* 1: also check every referenced page id on the device   */

@@ -148,4 +148,27 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* total, int* wave
   return before + x - v;
 }
 
+// 64-bit version of block_exclusive_scan (wave_tot: 16 slots).
+__device__ __forceinline__ long long block_exclusive_scan64(long long v, long long* total, long long* wave_tot) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  long long x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const long long y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wave_tot[wave] = x;
+  __syncthreads();
+  long long before = 0, all = 0;
+  const int nw = blockDim.x >> 6;
+  for (int w = 0; w < nw; ++w) {
+    const long long t = wave_tot[w];
+    if (w < wave) before += t;
+    all += t;
+  }
+  __syncthreads();
+  *total = all;
+  return before + x - v;
+}
+
 }  // namespace rl

@@ -26,11 +26,12 @@ namespace rl {
 
 namespace {
 
-constexpr int kMinSplit = 256;     // smallest automatic split (keys)
+constexpr int kMinSplit = 256;     // smallest automatic split of shared keys
+constexpr int kMinWorkerKeys = 256; // fewest keys per private-pass worker (automatic)
 constexpr int kTile = 32;          // keys per inner iteration of the private kernel
 constexpr int kGroupMax = 1024;    // batches up to this size get trajectory-group detection
 constexpr int kIntMax = 0x7fffffff;
-constexpr int kXcds = 8;
+constexpr int kHashBits = 11;     // planner hash table: 2048 slots for up to kGroupMax first page ids
 
 __device__ __forceinline__ int clamp_len(int L, int max_tokens, int* bad) {
   if (L < 0 || L > max_tokens) {
@@ -42,36 +43,47 @@ __device__ __forceinline__ int clamp_len(int L, int max_tokens, int* bad) {
 
 __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
+// Slot of first page ids in the planner's hash table (multiplicative hashing).
+__device__ __forceinline__ int page_hash(int key) { return (int)(((uint32_t)key * 2654435761u) >> (32 - kHashBits)); }
+
 __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
-  __shared__ int sL[kGroupMax], sP0[kGroupMax], sLead[kGroupMax], sKmin[kGroupMax], sCnt[kGroupMax],
-      sSg[kGroupMax];
+  __shared__ int sL[kGroupMax], sLead[kGroupMax], sKmin[kGroupMax], sCnt[kGroupMax], sSg[kGroupMax];
+  __shared__ int hKey[1 << kHashBits], hMin[1 << kHashBits];
   __shared__ int wave_tot[16];
   __shared__ long long wsum[16];
-  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int tid = threadIdx.x, nthr = blockDim.x, lane = tid & 63, wave = tid >> 6, nwaves = nthr >> 6;
   const int lg = a.kv.log2_page, P = a.kv.page_size;
   const int max_tokens = a.kv.max_pages * P;
-  const bool grouping = a.group_cap >= 2 && a.B <= kGroupMax;
+  // small batches (one sequence per thread) keep per-sequence state in LDS
+  // and get trajectory-group detection
+  const bool small = a.B <= kGroupMax;
+  const bool grouping = a.group_cap >= 2 && small;
   const uint32_t bt_sj = (uint32_t)a.kv.bt_sj;
   int bad = 0;
 
-  // lengths, their sum, and each sequence's first page id (when it has a full page)
+  if (grouping)
+    for (int i = tid; i < (1 << kHashBits); i += nthr) {
+      hKey[i] = -1;
+      hMin[i] = kIntMax;
+    }
+  // lengths and their sum
   long long sum = 0;
   for (int b = tid; b < a.B; b += nthr) {
     const int L = clamp_len(a.lens[b * a.lens_s], max_tokens, &bad);
     sum += L;
-    if (grouping) {
+    if (small) {
       sL[b] = L;
-      sP0[b] = (L >> lg) > 0 ? a.kv.bt[(int64_t)b * a.kv.bt_sb] : -1 - b;
       sKmin[b] = kIntMax;
       sCnt[b] = 0;
+      sLead[b] = b;
     }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
-  if ((tid & 63) == 0) wsum[tid >> 6] = sum;
+  if (lane == 0) wsum[wave] = sum;
   __syncthreads();
   long long total = 0;
-  for (int w = 0; w < (nthr >> 6); ++w) total += wsum[w];
+  for (int w = 0; w < nwaves; ++w) total += wsum[w];
 
   int C = a.forced_split;
   if (C <= 0) {
@@ -81,30 +93,50 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
   }
 
   if (grouping) {
-    // leader = lowest-indexed sequence with the same first page id
-    for (int b = tid; b < a.B; b += nthr) {
-      int lead = b;
-      const int key = sP0[b];
-      if (key >= 0)
-        for (int j = 0; j < b; ++j)
-          if (sP0[j] == key) {
-            lead = j;
-            break;
-          }
-      sLead[b] = lead;
+    // leader = lowest-indexed sequence with the same first page id, found
+    // through an LDS hash table keyed by that id (open addressing)
+    const int b = tid;
+    const int key = (b < a.B && (sL[b] >> lg) > 0) ? a.kv.bt[(int64_t)b * a.kv.bt_sb] : -1;
+    if (key >= 0) {
+      int h = page_hash(key);
+      for (;;) {
+        const int prev = atomicCAS(&hKey[h], -1, key);
+        if (prev == -1 || prev == key) {
+          atomicMin(&hMin[h], b);
+          break;
+        }
+        h = (h + 1) & ((1 << kHashBits) - 1);
+      }
     }
     __syncthreads();
-    // leading full pages each member shares with its leader; the group shares the minimum
-    for (int b = tid; b < a.B; b += nthr) {
-      const int lead = sLead[b];
-      if (lead == b) continue;
-      const int lim = min(sL[b], sL[lead]) >> lg;
-      const int* rb = a.kv.bt + (int64_t)b * a.kv.bt_sb;
+    if (key >= 0) {
+      int h = page_hash(key);
+      while (hKey[h] != key) h = (h + 1) & ((1 << kHashBits) - 1);
+      sLead[b] = hMin[h];
+    }
+    __syncthreads();
+    // leading full pages each member shares with its leader (one wave per
+    // member, 64 pages per comparison); the group shares the minimum
+    for (int m = wave; m < a.B; m += nwaves) {
+      const int lead = sLead[m];
+      if (lead == m) continue;
+      const int lim = min(sL[m], sL[lead]) >> lg;
+      const int* rb = a.kv.bt + (int64_t)m * a.kv.bt_sb;
       const int* rl = a.kv.bt + (int64_t)lead * a.kv.bt_sb;
-      int k = 0;
-      while (k < lim && rb[__umul24((uint32_t)k, bt_sj)] == rl[__umul24((uint32_t)k, bt_sj)]) ++k;
-      atomicMin(&sKmin[lead], k);
-      atomicAdd(&sCnt[lead], 1);
+      int k = lim;
+      for (int c = 0; c < lim; c += 64) {
+        const int kk = c + lane;
+        const bool differ = kk < lim && rb[__umul24((uint32_t)kk, bt_sj)] != rl[__umul24((uint32_t)kk, bt_sj)];
+        const unsigned long long mask = __builtin_amdgcn_ballot_w64(differ);
+        if (mask) {
+          k = c + __builtin_ctzll(mask);
+          break;
+        }
+      }
+      if (lane == 0) {
+        atomicMin(&sKmin[lead], k);
+        atomicAdd(&sCnt[lead], 1);
+      }
     }
     __syncthreads();
   }
@@ -127,34 +159,63 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
     __syncthreads();
   }
 
-  // per sequence: slots, private items, sub-group membership
-  int slot_off = 0, item_off = 0;
+  // Private keys, counted in tiles of kTile keys (each sequence's range is
+  // rounded up to whole tiles, so every piece starts on a tile boundary):
+  // prefix sums per sequence, then the number of workers (a worker takes W / n
+  // tiles, at least kMinWorkerKeys keys or the forced split, and at most
+  // max_workers of them run)
+  __syncthreads();   // the sum's per-wave totals are read before they are reused
+  long long poff = 0;
+  for (int b0 = 0; b0 < a.B; b0 += nthr) {
+    const int b = b0 + tid;
+    long long priv = 0;
+    if (b < a.B) {
+      int dummy = 0;
+      const int L = small ? sL[b] : clamp_len(a.lens[b * a.lens_s], max_tokens, &dummy);
+      priv = ceil_div(L - shared_keys(b), kTile);
+    }
+    long long tot;
+    const long long ex = poff + block_exclusive_scan64(priv, &tot, wsum);
+    if (b < a.B) a.ws.pref[b] = ex;
+    poff += tot;
+  }
+  const long long W = poff;
+  int nwork = 1;
+  if (W > 0) {
+    const long long per = (a.forced_split > 0 ? a.forced_split : kMinWorkerKeys) / kTile;
+    const long long n = (W + per - 1) / per;
+    nwork = (int)(n < a.max_workers ? n : a.max_workers);
+  }
+  if (tid == 0) a.ws.pref[a.B] = W;
+  __syncthreads();   // prefix sums visible to the workgroup
+  // workers whose share starts before tile y of the concatenation (0 < y <= W)
+  auto starts_before = [&](long long y) -> long long { return (y * nwork + W - 1) / W; };
+
+  // Per sequence: its shared splits, then one private piece per worker share
+  // it overlaps (a worker start strictly inside the range begins a new piece)
+  int slot_off = 0;
   for (int b0 = 0; b0 < a.B; b0 += nthr) {
     const int b = b0 + tid;
     int L = 0, S = 0, nsh = 0, npriv = 0, nslots = 0;
-    bool direct = false;
+    bool direct = false, empty = false;
     if (b < a.B) {
       int dummy = 0;
-      L = grouping ? sL[b] : clamp_len(a.lens[b * a.lens_s], max_tokens, &dummy);
+      L = small ? sL[b] : clamp_len(a.lens[b * a.lens_s], max_tokens, &dummy);
       S = shared_keys(b);
-      const int priv = L - S;
       nsh = S > 0 ? ceil_div(S, C) : 0;
-      npriv = priv > 0 ? ceil_div(priv, C) : (S > 0 ? 0 : 1);
+      const long long p0 = a.ws.pref[b], p1 = a.ws.pref[b + 1];
+      npriv = p1 > p0 ? (int)(1 + starts_before(p1) - starts_before(p0 + 1)) : 0;
+      empty = L == 0;
       direct = S == 0 && npriv == 1;
-      nslots = direct ? 0 : nsh + npriv;
+      nslots = direct || empty ? 0 : nsh + npriv;
     }
-    int slot_tot, item_tot;
+    int slot_tot;
     const int slot_base = slot_off + block_exclusive_scan(nslots, &slot_tot, wave_tot);
-    const int item_base = item_off + block_exclusive_scan(npriv, &item_tot, wave_tot);
     if (b < a.B) {
-      a.ws.nparts[b] = slot_base + nslots <= a.max_slots ? nslots : 0;
+      const bool fits = slot_base + nslots <= a.max_slots;
+      a.ws.nparts[b] = empty ? -1 : (fits ? nslots : 0);
       a.ws.base[b] = slot_base;
-      for (int s = 0; s < npriv; ++s) {
-        const int idx = item_base + s;
-        const int t0 = S + s * C;
-        const int slot = direct ? -1 : slot_base + nsh + s;
-        if (idx < a.max_items && slot < a.max_slots) a.ws.items[idx] = make_int4(b, t0, min(L, t0 + C), slot);
-      }
+      a.ws.seqs[b] = make_int4(S, direct || !fits ? -1 : slot_base + nsh, L, fits ? 1 : 0);
       if (S > 0) {
         const int lead = sLead[b];
         int rank = 0;
@@ -166,7 +227,6 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
       }
     }
     slot_off += slot_tot;
-    item_off += item_tot;
   }
   __syncthreads();
 
@@ -185,7 +245,7 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
   }
   if (tid == 0) {
     a.ws.hdr[0] = C;
-    a.ws.hdr[1] = min(item_off, a.max_items);
+    a.ws.hdr[1] = nwork;
     a.ws.hdr[2] = min(sitem_off, a.max_items);
     a.ws.hdr[3] = n_sg;
   }
@@ -205,6 +265,37 @@ __device__ __forceinline__ HeadResult finish(float m_log2, float l) {
   return r;
 }
 
+// Calls f(b, first key, end key, slot) for each piece of worker w's share of
+// the concatenated private key ranges (see the planner): the share is cut at
+// sequence boundaries; a piece that starts at a worker boundary inside a
+// sequence is that sequence's k-th private piece, k counting the worker
+// starts inside its range up to this one.
+template <typename F>
+__device__ __forceinline__ void for_each_piece(const DecodeArgs& a, int w, F&& f) {
+  const int n = a.ws.hdr[1];
+  if (w >= n) return;
+  const long long W = a.ws.pref[a.B];
+  long long x = (long long)w * W / n;
+  const long long x_end = (long long)(w + 1) * W / n;
+  if (x >= x_end) return;
+  int lo = 0, hi = a.B - 1;   // first sequence whose range ends after x
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (a.ws.pref[mid + 1] > x) hi = mid; else lo = mid + 1;
+  }
+  for (int b = lo; x < x_end; ++b) {
+    const long long p0 = a.ws.pref[b], p1 = a.ws.pref[b + 1];
+    if (p1 <= x) continue;
+    const long long e = p1 < x_end ? p1 : x_end;
+    const int4 sq = a.ws.seqs[b];   // (S, first private slot or -1, L, slots fit)
+    int slot = sq.y;
+    if (slot >= 0 && x > p0) slot += w - (int)(((p0 + 1) * n + W - 1) / W) + 1;
+    const int t_end = sq.x + (int)((e - p0) * kTile);
+    f(b, sq.x + (int)((x - p0) * kTile), t_end < sq.z ? t_end : sq.z, slot);
+    x = e;
+  }
+}
+
 // Split-KV decode on MFMA for a packed GQA group of up to 16 query heads.
 // One wave per (private item, KV head, 16-head block). Keys are processed 32
 // at a time: K goes straight from HBM into A-operand registers (each lane
@@ -220,22 +311,13 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
   const int per_item = a.Hkv * nqb;
   const int wpg = a.item_waves;             // waves per workgroup; divides per_item
   const int nch = per_item / wpg;
-  // Workgroup x runs on XCD x % 8; give each XCD a contiguous range of
-  // (item, wave group) pairs.
-  const int total = a.ws.hdr[1] * nch;
-  const int per_xcd = (total + kXcds - 1) / kXcds;
-  const int jx = blockIdx.x / kXcds;
-  if (jx >= per_xcd) return;
-  const int lin = (blockIdx.x % kXcds) * per_xcd + jx;
-  if (lin >= total) return;
-  const int item = lin / nch;
+  // workgroup -> (worker, wave group); a worker's wave groups take the same keys
+  const int worker = blockIdx.x / nch;
   const int wave = threadIdx.x >> 6;
-  const int rem = (lin - item * nch) * wpg + wave;
+  const int rem = (blockIdx.x - worker * nch) * wpg + wave;
   VTile& vs = reinterpret_cast<VTile*>(vs_dyn)[wave];
   const int g = rem % a.Hkv;
   const int qb = rem / a.Hkv;
-  const int4 it = a.ws.items[item];
-  const int b = it.x, t_begin = it.y, t_end = it.z, slot = it.w;
   int bad = 0;
 
   const int lane = threadIdx.x & 63;
@@ -245,6 +327,7 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
   const bool col_ok = col < nrows;
   const int h = g * a.R + row0 + (col_ok ? col : 0);
 
+  for_each_piece(a, worker, [&](int b, int t_begin, int t_end, int slot) {
   bf16x8 qv[4];
   {
     const __bf16* qp = (const __bf16*)a.q + (int64_t)b * a.q_sb + (int64_t)h * a.q_sh + grp * 8;
@@ -385,6 +468,7 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
       if (grp == 0) a.ws.part_lse[(int64_t)slot * a.Hq + h] = res.lse;
     }
   }
+  });
   if (bad) atomicOr(a.ws.err, kErrPage);
 }
 
@@ -392,16 +476,14 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
 // 16-lane group takes one key per step (a whole 256-byte row per load), keeps
 // its own online-softmax state, and the four groups are merged at the end.
 __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
-  const int item = blockIdx.x / a.Hkv;
-  const int g = blockIdx.x - item * a.Hkv;
-  if (item >= a.ws.hdr[1]) return;
-  const int4 it = a.ws.items[item];
-  const int b = it.x, t_begin = it.y, t_end = it.z, slot = it.w;
+  const int worker = blockIdx.x / a.Hkv;
+  const int g = blockIdx.x - worker * a.Hkv;
   int bad = 0;
   const int lane = threadIdx.x;
   const int c16 = lane & 15, grp = lane >> 4;
   const int h = g;  // R == 1
 
+  for_each_piece(a, worker, [&](int b, int t_begin, int t_end, int slot) {
   const float sl2 = a.scale * kLog2e;
   float qf[8];
   {
@@ -464,6 +546,7 @@ __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
       if (c16 == 0) a.ws.part_lse[(int64_t)slot * a.Hq + h] = res.lse;
     }
   }
+  });
   if (bad) atomicOr(a.ws.err, kErrPage);
 }
 
@@ -564,11 +647,13 @@ __global__ __launch_bounds__(64) void combine_kernel(DecodeArgs a) {
   const int b = blockIdx.x / a.Hq;
   const int h = blockIdx.x - b * a.Hq;
   const int n = a.ws.nparts[b];
-  if (n <= 0) return;
-  const int base = a.ws.base[b];
-  float r[2], lse_v;
-  merge_parts(a.ws.part_o + ((int64_t)base * a.Hq + h) * kHeadDim, (int64_t)a.Hq * kHeadDim,
-              a.ws.part_lse + (int64_t)base * a.Hq + h, a.Hq, n, r, &lse_v);
+  if (n == 0) return;     // written directly by its only piece
+  float r[2] = {0.f, 0.f}, lse_v = kNegInf;   // an empty sequence (n < 0): zeros, -inf
+  if (n > 0) {
+    const int base = a.ws.base[b];
+    merge_parts(a.ws.part_o + ((int64_t)base * a.Hq + h) * kHeadDim, (int64_t)a.Hq * kHeadDim,
+                a.ws.part_lse + (int64_t)base * a.Hq + h, a.Hq, n, r, &lse_v);
+  }
   const int lane = threadIdx.x;
   if (a.out_f32) {
     float* op = (float*)a.out + (int64_t)b * a.out_sb + (int64_t)h * a.out_sh + 2 * lane;
@@ -611,16 +696,29 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream, KernelTimer* t
   if (a.group_cap >= 2) prefix_kernel<<<(unsigned)a.prefix_grid, kPrefixWaves * 64, 0, stream>>>(a);
   if (timer) (void)hipEventRecord(timer->start, stream);
   if (a.R == 1) {
-    decode_valu_kernel<<<(unsigned)a.max_items * per_item, 64, 0, stream>>>(a);
+    decode_valu_kernel<<<(unsigned)a.max_workers * per_item, 64, 0, stream>>>(a);
   } else {
     const unsigned nch = per_item / a.item_waves;
-    const unsigned grid = (unsigned)(((int64_t)a.max_items * nch + kXcds - 1) / kXcds * kXcds);
+    const unsigned grid = (unsigned)((int64_t)a.max_workers * nch);
     const size_t lds = (size_t)a.item_waves * kTile * (kHeadDim + 8) * sizeof(u16);
     decode_mfma_kernel<<<grid, 64 * a.item_waves, lds, stream>>>(a);
   }
   if (timer) (void)hipEventRecord(timer->stop, stream);
   combine_kernel<<<(unsigned)(a.B * a.Hq), 64, 0, stream>>>(a);
   return hipGetLastError();
+}
+
+int decode_workers_per_cu(int R, int Hkv, int item_waves) {
+  int blocks = 0;
+  if (R == 1) {
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_valu_kernel, 64, 0) != hipSuccess) blocks = 0;
+    return blocks / Hkv > 1 ? blocks / Hkv : 1;
+  }
+  const size_t lds = (size_t)item_waves * kTile * (kHeadDim + 8) * sizeof(u16);
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_mfma_kernel, 64 * item_waves, lds) != hipSuccess)
+    blocks = 0;
+  const int nch = Hkv * ((R + 15) / 16) / item_waves;
+  return blocks / nch > 1 ? blocks / nch : 1;
 }
 
 hipError_t launch_merge(const MergeArgs& a, hipStream_t stream) {

@@ -25,16 +25,21 @@ struct PagedKV {
   int num_pages, page_size, log2_page, max_pages;
 };
 
-// Workspace carve-up of one decode call. Work items: private items cover a
-// key range of one sequence; shared items cover the prefix pages a trajectory
-// group shares and serve every member of one sub-group (at most 128 query
-// rows). Partial results live in "slots"; sequence b owns slots
-// base[b] .. base[b] + nparts[b] - 1 (nparts[b] == 0: written directly).
+// Workspace carve-up of one decode call. Private keys: sequence b owns
+// [pref[b], pref[b+1]) of the concatenation of all sequences' private key
+// ranges (its keys S_b .. L_b - 1), and worker w of n takes the equal share
+// [w W / n, (w+1) W / n) of it, cut at sequence boundaries into pieces.
+// Shared items cover the prefix pages a trajectory group shares and serve
+// every member of one sub-group (at most 128 query rows). Partial results
+// live in "slots"; sequence b owns slots base[b] .. base[b] + nparts[b] - 1:
+// its shared splits, then its private pieces in key order (nparts[b] == 0:
+// one piece, written directly; -1: an empty sequence, written by the combine).
 struct DecodePlanWs {
-  int* hdr;        // [0] split tokens C, [1] private items, [2] shared items, [3] sub-groups
+  int* hdr;        // [0] split tokens C of shared keys, [1] workers, [2] shared items, [3] sub-groups
   int* nparts;     // [B]
   int* base;       // [B]
-  int4* items;     // [max_items] (sequence, first key, end key, slot or -1 for a direct write)
+  long long* pref; // [B + 1] prefix sums of private keys
+  int4* seqs;      // [B] (shared keys S, slot of the first private piece or -1 for a direct write, L, 0)
   int4* sitems;    // [max_items] (sub-group, first key, end key, split index)
   int4* sgroups;   // [B] (sequence whose block table is read, members, shared keys, shared splits)
   int* sg_members; // [B * group_cap] member sequences of each sub-group
@@ -57,8 +62,9 @@ struct DecodeArgs {
   float* lse;             // nullable
   int64_t lse_sb, lse_sh;
   int forced_split;       // 0 = choose on device
-  int target_items;       // work items the device planner aims for
-  int max_items;          // capacity of each item list
+  int target_items;       // shared splits the device planner aims for
+  int max_items;          // capacity of the shared item list
+  int max_workers;        // workers the private pass may use (its grid / workgroups per worker)
   int max_slots;          // capacity of the partial buffers
   int group_cap;          // members per sub-group (128 query rows / R), 0 = no prefix sharing
   int prefix_grid;        // workgroups of the group-prefix pass (grid-stride over its work)
@@ -116,6 +122,9 @@ struct KernelTimer {
 };
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream, KernelTimer* timer);
+// Workers of the private decode pass that are resident on one CU at a time
+// (from the kernel's occupancy; a worker is one workgroup per wave group).
+int decode_workers_per_cu(int R, int Hkv, int item_waves);
 hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream, KernelTimer* timer);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t stream);
 

@@ -42,6 +42,7 @@ struct EnvDefaults {
   int prefix_share = RL_PREFIX_AUTO;
   int validate = 0;
   int target_wgs_per_cu = 64;
+  int workers_per_cu = 0;   // 0: as many as are resident at once
   bool fail_alloc = false;
 };
 
@@ -52,6 +53,7 @@ const EnvDefaults& env() {
     if (const char* s = std::getenv("RL_ATTN_PREFIX_SHARE")) e.prefix_share = std::strcmp(s, "off") == 0;
     if (const char* s = std::getenv("RL_ATTN_VALIDATE")) e.validate = std::atoi(s) != 0;
     if (const char* s = std::getenv("RL_ATTN_TARGET_WGS_PER_CU")) e.target_wgs_per_cu = std::max(1, std::atoi(s));
+    if (const char* s = std::getenv("RL_ATTN_WORKERS_PER_CU")) e.workers_per_cu = std::max(0, std::atoi(s));
     if (const char* s = std::getenv("RL_ATTN_TEST_FAIL_ALLOC")) e.fail_alloc = std::atoi(s) != 0;
     return e;
   }();
@@ -245,12 +247,13 @@ void prof_commit(int kind, rl::KernelTimer* t) {
 
 // ------------------------------------------------------------------- decode
 // Capacities (see the planner): with split size C and T = sum(L) / C,
-// private items <= T + B, shared items <= T + B, partial slots <= T + 2B.
-// An automatic C keeps T at or below the target item count; a forced C
-// bounds T by B * ceil(max_pages * P / C).
+// Private pieces <= workers + B, shared items <= T + B, partial slots <=
+// workers + T + 2B. An automatic shared split C keeps T at or below the target
+// item count; a forced C bounds T by B * ceil(max_pages * P / C) and lets the
+// private pass use up to that many workers of C keys.
 struct DecodeLayout {
-  int max_items, max_slots, group_cap;
-  size_t off_nparts, off_base, off_items, off_sitems, off_sgroups, off_members, off_po, off_pl, total;
+  int max_items, max_slots, max_workers, group_cap;
+  size_t off_nparts, off_base, off_pref, off_seqs, off_sitems, off_sgroups, off_members, off_po, off_pl, total;
 };
 
 int64_t decode_wgs_per_item(int64_t Hq, int64_t Hkv) {
@@ -258,8 +261,32 @@ int64_t decode_wgs_per_item(int64_t Hq, int64_t Hkv) {
   return Hkv * (R == 1 ? 1 : (R + 15) / 16);
 }
 
+// waves of one decode workgroup: the largest divisor of the item's waves (its
+// KV heads and 16-head blocks) up to 8, so a workgroup reads whole token rows
+int decode_item_waves(int64_t Hq, int64_t Hkv) {
+  const int64_t R = Hq / std::max<int64_t>(1, Hkv);
+  const int per_item = (int)(Hkv * ((R + 15) / 16));
+  for (int w = std::min(per_item, 8); w >= 1; --w)
+    if (per_item % w == 0) return w;
+  return 1;
+}
+
 int target_items_for(int64_t Hq, int64_t Hkv, int cus) {
   return (int)std::max<int64_t>(1, (int64_t)cus * env().target_wgs_per_cu / decode_wgs_per_item(Hq, Hkv));
+}
+
+// workers of the private pass resident on one CU (cached per shape)
+int workers_per_cu(int64_t Hq, int64_t Hkv) {
+  if (env().workers_per_cu > 0) return env().workers_per_cu;
+  static std::mutex mu;
+  static std::map<std::pair<int64_t, int64_t>, int> cache;
+  std::lock_guard<std::mutex> lk(mu);
+  auto it = cache.find({Hq, Hkv});
+  if (it != cache.end()) return it->second;
+  const int R = (int)(Hq / std::max<int64_t>(1, Hkv));
+  const int n = rl::decode_workers_per_cu(R, (int)Hkv, decode_item_waves(Hq, Hkv));
+  cache[{Hq, Hkv}] = n;
+  return n;
 }
 
 DecodeLayout decode_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t max_pages, int64_t P, int split, int cus,
@@ -269,16 +296,20 @@ DecodeLayout decode_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t max_pages
   const int64_t max_tokens = max_pages * P;
   const int64_t T = split > 0 ? B * std::max<int64_t>(1, (max_tokens + split - 1) / split)
                               : (int64_t)target_items_for(Hq, Hkv, cus);
+  const int64_t workers = split > 0 ? T : (int64_t)cus * workers_per_cu(Hq, Hkv);
   L.max_items = (int)std::min<int64_t>(T + B, INT32_MAX / 2);
-  L.max_slots = (int)std::min<int64_t>(T + 2 * B, INT32_MAX / 2);
+  L.max_workers = (int)std::min<int64_t>(std::max<int64_t>(1, workers), INT32_MAX / 64);
+  L.max_slots = (int)std::min<int64_t>(L.max_workers + T + 2 * B, INT32_MAX / 2);
   L.group_cap = (prefix_share && R <= 64) ? (int)(128 / R) : 0;
   size_t off = 256;  // header
   L.off_nparts = off;
   off += align256(B * 4);
   L.off_base = off;
   off += align256(B * 4);
-  L.off_items = off;
-  off += align256((size_t)L.max_items * 16);
+  L.off_pref = off;
+  off += align256((size_t)(B + 1) * 8);
+  L.off_seqs = off;
+  off += align256((size_t)B * 16);
   L.off_sitems = off;
   off += align256((size_t)L.max_items * 16);
   L.off_sgroups = off;
@@ -421,23 +452,16 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   a.target_items = target_items_for(Hq, Hkv, cus);
   a.max_items = lay.max_items;
   a.max_slots = lay.max_slots;
+  a.max_workers = lay.max_workers;
   a.group_cap = lay.group_cap;
   a.prefix_grid = 2 * cus;
-  {
-    // the waves of one work item (its KV heads and 16-head blocks) share a workgroup
-    const int per_item = (int)(Hkv * ((a.R + 15) / 16));
-    a.item_waves = 1;
-    for (int w = std::min(per_item, 8); w >= 1; --w)
-      if (per_item % w == 0) {
-        a.item_waves = w;
-        break;
-      }
-  }
+  a.item_waves = decode_item_waves(Hq, Hkv);
   a.validate = o.validate;
   a.ws.hdr = reinterpret_cast<int*>(base);
   a.ws.nparts = reinterpret_cast<int*>(base + lay.off_nparts);
   a.ws.base = reinterpret_cast<int*>(base + lay.off_base);
-  a.ws.items = reinterpret_cast<int4*>(base + lay.off_items);
+  a.ws.pref = reinterpret_cast<long long*>(base + lay.off_pref);
+  a.ws.seqs = reinterpret_cast<int4*>(base + lay.off_seqs);
   a.ws.sitems = reinterpret_cast<int4*>(base + lay.off_sitems);
   a.ws.sgroups = reinterpret_cast<int4*>(base + lay.off_sgroups);
   a.ws.sg_members = reinterpret_cast<int*>(base + lay.off_members);
