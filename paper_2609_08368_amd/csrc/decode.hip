@@ -156,7 +156,17 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
     if (b < a.B && sLead[b] == b && shared_keys(b) > 0) nsub = ceil_div(sCnt[b] + 1, cap);
     const int excl = block_exclusive_scan(nsub, &n_sg, wave_tot);
     if (b < a.B) sSg[b] = excl;
-    __syncthreads();
+    // Split of the shared keys: at least C, and large enough that the shared
+    // items of all sub-groups times the KV heads fit the group-prefix grid in
+    // one round (its workgroups are all resident; a second, partly filled
+    // round would double the pass's time)
+    long long tot_sh;
+    (void)block_exclusive_scan64(nsub > 0 ? (long long)nsub * shared_keys(b) : 0, &tot_sh, wsum);
+    if (a.forced_split <= 0 && tot_sh > 0) {
+      long long per = (tot_sh * a.Hkv + a.prefix_grid - 1) / a.prefix_grid;
+      per = (per + 63) & ~63LL;
+      if (per > C) C = (int)per;
+    }
   }
 
   // Private keys, counted in tiles of kTile keys (each sequence's range is
