@@ -176,3 +176,29 @@ def test_decode_group_prefix_shuffled_batch():
     # both runs agree with each other everywhere at the path's tolerance (each is a
     # bf16-rounded result, so they differ by up to twice the per-side error)
     H.compare(out, H.f64(out_off), what="shared vs unshared")
+
+
+def test_decode_many_sequences():
+    """More sequences than the planner keeps in LDS (1,500 > 1,024): per-sequence state
+    goes through chunked scans, with no group detection."""
+    rng = np.random.default_rng(21)
+    lens = rng.integers(0, 200, size=1500).tolist()
+    w = wl.custom(21, "decode", lens, hq=8, hkv=2, page_size=16)
+    H.say("1500 sequences")
+    t = wl.materialize(w, DEV)
+    for split in (0, 64):
+        out, lse = H.run_decode(w, t, split_tokens=split)
+        ref_o, ref_l = H.oracle_full(w, t)
+        H.compare(out, ref_o, lse, ref_l, what=f"1500 sequences split={split}")
+
+
+@pytest.mark.parametrize("split", [64, 128, 256])
+def test_decode_worker_shares_span_sequences(split):
+    """Worker shares that start and end inside sequences and cover many short ones."""
+    lens = [1] * 40 + [1000] + [33, 31, 32, 64, 65, 0, 5] * 6 + [700]
+    w = wl.custom(22, "decode", lens, hq=16, hkv=2, page_size=32)
+    H.say(f"worker shares split={split}")
+    t = wl.materialize(w, DEV)
+    out, lse = H.run_decode(w, t, split_tokens=split)
+    ref_o, ref_l = H.oracle_full(w, t)
+    H.compare(out, ref_o, lse, ref_l, what=f"worker shares split={split}")

@@ -86,3 +86,14 @@ def test_extend_full_size_sampled():
         H.say(f"  seq {seq} kv={int(w.kv_lens[seq])} n={n} rows={rows} {res}")
     del t
     torch.cuda.empty_cache()
+
+
+def test_extend_determinism():
+    """Run-to-run identical results, on both page-addressing paths."""
+    for ps in (16, 64):
+        w = wl.custom(23, "extend", [700, 250, 90], q_lens=[300, 250, 1], hq=16, hkv=2, page_size=ps)
+        H.say(f"extend determinism P={ps}")
+        t = wl.materialize(w, DEV)
+        outs = [H.run_extend(w, t)[0] for _ in range(3)]
+        for o in outs[1:]:
+            assert torch.equal(o.view(torch.int16), outs[0].view(torch.int16)), "run-to-run results differ"
