@@ -81,27 +81,93 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def pmc_workload():
-    """What the counter runs profile: three ragged-64K decode calls and three
-    copies of CALIB_BYTES (the calibration kernel for FETCH_SIZE / WRITE_SIZE)."""
+def pmc_workload(kind: str = "ragged"):
+    """What the counter runs profile.
+
+    ragged: three ragged-64K decode calls, then three copies of CALIB_BYTES (the
+    calibration kernel for FETCH_SIZE / WRITE_SIZE); extend: two multi-turn extend
+    calls; group / group-noshare: three decode calls of the 16x8 trajectory-group
+    batch with prefix sharing on / off, then the same calibration copies."""
     import torch
 
     from paper_2609_08368_amd import rl_attn as ra
     from paper_2609_08368_amd import workloads as wl
 
     dev = torch.device("cuda:0")
-    w = wl.decode_ragged()
+    w = {"ragged": wl.decode_ragged, "extend": wl.extend_multiturn}.get(kind, wl.decode_group_prefix)()
     t = wl.materialize(w, dev, poison=False)
     out = torch.empty_like(t["q"])
+    if kind == "extend":
+        for _ in range(2):
+            ra.extend_plain(t["q"], t["qo_indptr"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"],
+                            t["scale"], out=out)
+        torch.cuda.synchronize()
+        print(json.dumps({"pmc_workload": kind, "flops": w.flops()}), flush=True)
+        return
+    share = {"prefix_share": kind != "group-noshare"}
     for _ in range(3):
-        ra.decode_plain(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out)
+        ra.decode(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out, **share)
     src = torch.empty(CALIB_BYTES // 2, dtype=torch.bfloat16, device=dev).fill_(1.0)
     dst = torch.empty_like(src)
     torch.cuda.synchronize()
     for _ in range(3):
         dst.copy_(src)
     torch.cuda.synchronize()
-    print(json.dumps({"pmc_workload": "done", "kv_bytes": w.kv_bytes(), "calib_bytes": CALIB_BYTES}), flush=True)
+    print(json.dumps({"pmc_workload": kind, "kv_bytes": w.kv_bytes(unique=True), "logical_kv_bytes": w.kv_bytes(),
+                      "calib_bytes": CALIB_BYTES}), flush=True)
+
+
+def prefix_study(steps: int = 20):
+    """Group-prefix decode with prefix sharing on and off: the 16x8 group batch
+    (4096 shared tokens) and its long-prompt variant (32768 shared tokens)."""
+    import torch
+
+    from paper_2609_08368_amd import rl_attn as ra
+    from paper_2609_08368_amd import workloads as wl
+
+    dev = torch.device("cuda:0")
+    res = {}
+    for w in (wl.decode_group_prefix(), wl.decode_group_long_prefix()):
+        t = wl.materialize(w, dev, poison=False)
+        out = torch.empty_like(t["q"])
+        row = {"unique_kv_bytes": w.kv_bytes(unique=True), "logical_kv_bytes": w.kv_bytes()}
+        for share in (True, False):
+            call = lambda: ra.decode(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"],
+                                     out=out, prefix_share=share)
+            for _ in range(3):
+                call()
+            torch.cuda.synchronize()
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            ev[0].record()
+            for _ in range(steps):
+                call()
+            ev[1].record()
+            torch.cuda.synchronize()
+            row["ms_share" if share else "ms_no_share"] = round(ev[0].elapsed_time(ev[1]) / steps, 4)
+        row["speedup"] = round(row["ms_no_share"] / row["ms_share"], 3)
+        res[w.name] = row
+        del t, out
+        torch.cuda.empty_cache()
+    print(json.dumps(res), flush=True)
+
+
+def summarize_counters(d: str):
+    """Per kernel and counter: dispatches and the mean value per dispatch (summed over
+    the counter's dimensions) of a rocprofv3 --pmc output directory."""
+    import csv
+    import glob
+
+    per = {}
+    for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(path)):
+            name = r["Kernel_Name"].replace("(anonymous namespace)::", "").split("(")[0]
+            key = (name, r["Counter_Name"], int(r["Dispatch_Id"]))
+            per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+    agg = {}
+    for (kern, ctr, _), v in per.items():
+        agg.setdefault((kern, ctr), []).append(v)
+    for (kern, ctr), vals in sorted(agg.items()):
+        print(f"{kern[-40:]:40s} {ctr:32s} dispatches {len(vals):3d}  mean {sum(vals) / len(vals):.6g}")
 
 
 def summarize_pmc(fetch_dir: str, write_dir: str):
@@ -166,7 +232,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--pmc-workload", action="store_true", help="run only what the counter runs profile")
+    ap.add_argument("--pmc-workload", nargs="?", const="ragged", choices=["ragged", "extend", "group", "group-noshare"],
+                    help="run only what a counter run profiles")
+    ap.add_argument("--summarize-counters", metavar="PMC_DIR", help="per-kernel means of a rocprofv3 --pmc run")
+    ap.add_argument("--prefix-study", action="store_true", help="time group-prefix decode with sharing on and off")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the HBM traffic summary from two rocprofv3 --pmc output directories")
     args = ap.parse_args()
@@ -174,7 +243,13 @@ def main():
         summarize_pmc(*args.summarize_pmc)
         return
     if args.pmc_workload:
-        pmc_workload()
+        pmc_workload(args.pmc_workload)
+        return
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters)
+        return
+    if args.prefix_study:
+        prefix_study()
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (the kernels run on one device's share; "

@@ -184,6 +184,17 @@ def extend_multiturn(seed: int = 1005) -> Paged:
                  pool, table, kv, chunk.astype(np.int32), poison)
 
 
+def decode_group_long_prefix(seed: int = 1006) -> Paged:
+    """The group-prefix batch with long prompts: 16 prompts x G=8, shared prefix of 32768 tokens
+    (far more than the GPU's last-level cache), private continuations U{512..4096}, 64/8 heads, page 64."""
+    rng = np.random.default_rng(seed)
+    shared = 32768
+    lens = (shared + rng.integers(512, 4096, size=128, endpoint=True)).astype(np.int32)
+    table, pool, poison = _assign_pages(rng, lens, 64, group_size=8, shared_tokens=shared)
+    return Paged("decode_group_long_prefix_16x8_shared32768_h64kv8_p64", "decode", seed, 64, 8, 64, pool,
+                 table, lens, np.ones(128, np.int32), poison, shared_prefix_pages=shared // 64, group_size=8)
+
+
 def custom(seed: int, kind: str, kv_lens, q_lens=None, hq: int = 8, hkv: int = 2, page_size: int = 16,
            pool_extra: int = 3, group_size: int = 1, shared_tokens: int = 0, kv_head_scale=None) -> Paged:
     """A small workload of any shape (tests)."""
