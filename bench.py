@@ -387,6 +387,20 @@ def main():
             "algorithmic_bytes": kv_dec,
         },
     }
+    # measured ceilings on this device, beside the specification peaks
+    del t_grp, t_ext
+    torch.cuda.empty_cache()
+    buf = torch.ones(4 << 30, dtype=torch.uint8, device=dev)
+    read_gbps = ra.diag_read_bandwidth(buf, reps=10)
+    del buf
+    loop_tflops = ra.diag_mfma_bf16(20000)
+    result["ceilings"] = {
+        "hbm_read_GBps": round(read_gbps, 1), "hbm_read_frac_of_spec": round(read_gbps / HBM_PEAK_GBPS, 4),
+        "decode_frac_of_read_ceiling": round(dec_gbps / read_gbps, 4),
+        "mfma_bf16_loop_TFLOPs": round(loop_tflops, 1),
+        "mfma_loop_frac_of_spec": round(loop_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+        "extend_frac_of_mfma_loop": round(ext_tflops / loop_tflops, 4),
+    }
     if not args.no_cpu_baseline:
         log("timing the oracle on host cores ...")
         result["cpu_baseline"] = cpu_baseline(w_dec, t_dec, args.cpu_budget)

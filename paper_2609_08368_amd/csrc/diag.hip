@@ -1,0 +1,81 @@
+// Measurement aids: a streaming read of a device buffer (the HBM read
+// ceiling) and a register-only loop of bf16 MFMAs (the matrix-core ceiling).
+#include <hip/hip_runtime.h>
+
+#include "attn_common.hpp"
+#include "kernels.hpp"
+
+namespace rl {
+namespace {
+
+constexpr int kReadThreads = 256;
+constexpr int kReadUnroll = 8;
+constexpr int kReadBlocksPerCu = 64;   // the fastest of 4..64 workgroups per CU (and unroll 4 / 8) measured
+
+// Grid-stride read of n16 16-byte words; the xor of everything read is stored
+// only when it equals a value no real buffer produces in practice, so the
+// loads stay live without a store per thread.
+__global__ __launch_bounds__(kReadThreads) void read_kernel(const uint4* p, size_t n16, unsigned* sink) {
+  unsigned acc = 0;
+  const size_t stride = (size_t)gridDim.x * kReadThreads;
+  size_t i = (size_t)blockIdx.x * kReadThreads + threadIdx.x;
+  for (; i + (kReadUnroll - 1) * stride < n16; i += kReadUnroll * stride) {
+    uint4 v[kReadUnroll];
+#pragma unroll
+    for (int u = 0; u < kReadUnroll; ++u) v[u] = p[i + u * stride];
+#pragma unroll
+    for (int u = 0; u < kReadUnroll; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  for (; i < n16; i += stride) {
+    const uint4 v = p[i];
+    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+  if (acc == 0x9e3779b9u) sink[0] = acc;
+}
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+constexpr int kMfmaThreads = 512;   // two waves per SIMD
+constexpr int kChains = 4;
+
+__global__ __launch_bounds__(kMfmaThreads) void mfma_kernel(int iters, float* sink) {
+  bf16x8 a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = (__bf16)(1e-3f * (float)(threadIdx.x & 63) + 1e-4f * (float)i);
+    b[i] = (__bf16)(2e-3f * (float)i);
+  }
+  f32x16 acc[kChains];
+#pragma unroll
+  for (int c = 0; c < kChains; ++c)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[c][e] = 0.f;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int k = 0; k < 32; ++k)
+      acc[k % kChains] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[k % kChains], 0, 0, 0);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < kChains; ++c)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s += acc[c][e];
+  if (s == 12345.678f) sink[0] = s;
+}
+
+}  // namespace
+
+hipError_t launch_diag_read(const void* buf, size_t bytes, unsigned* sink, int cus, hipStream_t stream) {
+  read_kernel<<<(unsigned)cus * kReadBlocksPerCu, kReadThreads, 0, stream>>>(static_cast<const uint4*>(buf), bytes / 16, sink);
+  return hipGetLastError();
+}
+
+hipError_t launch_diag_mfma(int iters, float* sink, int cus, hipStream_t stream) {
+  mfma_kernel<<<(unsigned)cus, kMfmaThreads, 0, stream>>>(iters, sink);
+  return hipGetLastError();
+}
+
+double diag_mfma_flops(int iters, int cus) {
+  return (double)cus * (kMfmaThreads / 64) * (double)iters * 32.0 * (2.0 * 32 * 32 * 16);
+}
+
+}  // namespace rl

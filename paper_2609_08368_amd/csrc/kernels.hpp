@@ -122,6 +122,12 @@ struct KernelTimer {
 };
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream, KernelTimer* timer);
+// Measurement aids (see rl_attn_diag.h): a grid-stride read of `bytes` and a
+// register-only bf16 MFMA loop.
+hipError_t launch_diag_read(const void* buf, size_t bytes, unsigned* sink, int cus, hipStream_t stream);
+hipError_t launch_diag_mfma(int iters, float* sink, int cus, hipStream_t stream);
+double diag_mfma_flops(int iters, int cus);
+
 // Workers of the private decode pass that are resident on one CU at a time
 // (from the kernel's occupancy; a worker is one workgroup per wave group).
 int decode_workers_per_cu(int R, int Hkv, int item_waves);

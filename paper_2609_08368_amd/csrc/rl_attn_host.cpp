@@ -17,6 +17,7 @@
 
 #include "kernels.hpp"
 #include "rl_attn.h"
+#include "rl_attn_diag.h"
 
 namespace {
 
@@ -706,6 +707,83 @@ size_t rl_attn_extend_workspace_size(int64_t batch, int64_t total_q, int64_t num
   if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0) return 0;
   int mi = 0;
   return extend_ws_bytes(batch, total_q, num_kv_heads, num_q_heads / num_kv_heads, &mi);
+}
+
+// ------------------------------------------------------------ measurement aids
+namespace {
+
+// A small device allocation released when the scope ends.
+struct DevBuf {
+  void* p = nullptr;
+  ~DevBuf() {
+    if (p) (void)hipFree(p);
+  }
+};
+
+}  // namespace
+
+int rl_attn_diag_read_bandwidth(const void* buf, int64_t bytes, int32_t reps, double* gb_per_s, void* stream) {
+  if (!buf || !gb_per_s) return fail(RL_ERR_INVALID_ARG, "diag_read_bandwidth: null pointer");
+  if (bytes <= 0 || bytes % 16 != 0) return fail(RL_ERR_INVALID_ARG, "diag_read_bandwidth: bytes must be a positive multiple of 16");
+  if ((reinterpret_cast<uintptr_t>(buf) & 15) != 0) return fail(RL_ERR_INVALID_ARG, "diag_read_bandwidth: buf must be 16-byte aligned");
+  if (reps < 1) return fail(RL_ERR_INVALID_ARG, "diag_read_bandwidth: reps must be >= 1");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  const int cus = device_cus(dev);
+  DevBuf sink;
+  if ((e = hipMalloc(&sink.p, 16)) != hipSuccess) return hip_fail(e, "hipMalloc");
+  hipEvent_t a = nullptr, b = nullptr;
+  if ((e = hipEventCreate(&a)) != hipSuccess) return hip_fail(e, "hipEventCreate");
+  if ((e = hipEventCreate(&b)) != hipSuccess) {
+    (void)hipEventDestroy(a);
+    return hip_fail(e, "hipEventCreate");
+  }
+  unsigned* sk = static_cast<unsigned*>(sink.p);
+  e = rl::launch_diag_read(buf, (size_t)bytes, sk, cus, st);
+  if (e == hipSuccess) e = hipEventRecord(a, st);
+  for (int r = 0; r < reps && e == hipSuccess; ++r) e = rl::launch_diag_read(buf, (size_t)bytes, sk, cus, st);
+  if (e == hipSuccess) e = hipEventRecord(b, st);
+  if (e == hipSuccess) e = hipEventSynchronize(b);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
+  (void)hipEventDestroy(a);
+  (void)hipEventDestroy(b);
+  if (e != hipSuccess) return hip_fail(e, "diag_read_bandwidth");
+  *gb_per_s = ms > 0.f ? (double)bytes * reps / (ms * 1e-3) / 1e9 : 0.0;
+  return RL_OK;
+}
+
+int rl_attn_diag_mfma_bf16(int64_t iters, double* tflop_per_s, void* stream) {
+  if (!tflop_per_s) return fail(RL_ERR_INVALID_ARG, "diag_mfma_bf16: null pointer");
+  if (iters < 1 || iters > (1 << 24)) return fail(RL_ERR_INVALID_ARG, "diag_mfma_bf16: iters must be in [1, 2^24]");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  const int cus = device_cus(dev);
+  DevBuf sink;
+  if ((e = hipMalloc(&sink.p, 16)) != hipSuccess) return hip_fail(e, "hipMalloc");
+  float* sk = static_cast<float*>(sink.p);
+  hipEvent_t a = nullptr, b = nullptr;
+  if ((e = hipEventCreate(&a)) != hipSuccess) return hip_fail(e, "hipEventCreate");
+  if ((e = hipEventCreate(&b)) != hipSuccess) {
+    (void)hipEventDestroy(a);
+    return hip_fail(e, "hipEventCreate");
+  }
+  e = rl::launch_diag_mfma((int)std::min<int64_t>(iters, 64), sk, cus, st);   // warm-up
+  if (e == hipSuccess) e = hipEventRecord(a, st);
+  if (e == hipSuccess) e = rl::launch_diag_mfma((int)iters, sk, cus, st);
+  if (e == hipSuccess) e = hipEventRecord(b, st);
+  if (e == hipSuccess) e = hipEventSynchronize(b);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
+  (void)hipEventDestroy(a);
+  (void)hipEventDestroy(b);
+  if (e != hipSuccess) return hip_fail(e, "diag_mfma_bf16");
+  *tflop_per_s = ms > 0.f ? rl::diag_mfma_flops((int)iters, cus) / (ms * 1e-3) / 1e12 : 0.0;
+  return RL_OK;
 }
 
 int rl_attn_profile_enable(int on) {

@@ -18,7 +18,8 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 # RL_ATTN_LIB selects another build of the library (A/B comparisons of builds)
 LIB_PATH = os.environ.get("RL_ATTN_LIB", os.path.join(_PKG, "librlattn.so"))
-HEADER = os.path.join(os.path.dirname(_PKG), "include", "rl_attn.h")
+INCLUDE = os.path.join(os.path.dirname(_PKG), "include")
+HEADER = os.path.join(INCLUDE, "rl_attn.h")
 
 RL_BF16, RL_F32, RL_I32 = 1, 2, 3
 RL_PREFIX_AUTO, RL_PREFIX_OFF = 0, 1
@@ -73,20 +74,27 @@ def lib() -> ctypes.CDLL:
         L.rl_attn_release.restype = None
         L.rl_attn_profile_enable.argtypes = [ctypes.c_int]
         L.rl_attn_profile_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double)]
+        dp = ctypes.POINTER(ctypes.c_double)
+        L.rl_attn_diag_read_bandwidth.argtypes = [vp, ctypes.c_int64, ctypes.c_int32, dp, vp]
+        L.rl_attn_diag_mfma_bf16.argtypes = [ctypes.c_int64, dp, vp]
         for name in ("rl_attn_decode", "rl_attn_extend", "rl_attn_decode_ex", "rl_attn_extend_ex",
                      "rl_attn_merge", "rl_attn_check_device_errors", "rl_attn_reserve_workspace",
-                     "rl_attn_profile_enable", "rl_attn_profile_read"):
+                     "rl_attn_profile_enable", "rl_attn_profile_read", "rl_attn_diag_read_bandwidth",
+                     "rl_attn_diag_mfma_bf16"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
 
 
 def header_functions() -> list:
-    """Names of the functions ``include/rl_attn.h`` declares."""
-    with open(HEADER) as f:
-        text = f.read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(rl_attn_\w+)\s*\(", text)))
+    """Names of the functions the headers under ``include/`` declare."""
+    names = set()
+    for fn in sorted(os.listdir(INCLUDE)):
+        if fn.endswith(".h"):
+            with open(os.path.join(INCLUDE, fn)) as f:
+                text = re.sub(r"/\*.*?\*/", "", f.read(), flags=re.S)
+            names.update(re.findall(r"\b(rl_attn_\w+)\s*\(", text))
+    return sorted(names)
 
 
 def last_error() -> str:
@@ -212,3 +220,18 @@ def profile_read(kind: str):
 
 def release():
     lib().rl_attn_release()
+
+
+def diag_read_bandwidth(buf: torch.Tensor, reps: int = 10, stream=None) -> float:
+    """HBM read rate (GB/s) of streaming ``buf`` (a device tensor) ``reps`` times."""
+    r = ctypes.c_double(0.0)
+    _check(lib().rl_attn_diag_read_bandwidth(ctypes.c_void_p(buf.data_ptr()), buf.numel() * buf.element_size(),
+                                            reps, ctypes.byref(r), _stream(stream)))
+    return r.value
+
+
+def diag_mfma_bf16(iters: int = 20000, stream=None) -> float:
+    """TFLOP/s of a register-only bf16 MFMA loop on every CU."""
+    t = ctypes.c_double(0.0)
+    _check(lib().rl_attn_diag_mfma_bf16(iters, ctypes.byref(t), _stream(stream)))
+    return t.value

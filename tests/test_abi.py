@@ -155,3 +155,15 @@ def test_scale_must_be_positive_and_finite(scale):
     rc = ra.lib().rl_attn_decode_ex(r(a["q"]), r(a["k"]), r(a["v"]), r(a["bt"]), r(a["lens"]), ctypes.c_float(scale),
                                     r(a["out"]), None, None, None)
     assert ra.STATUS[rc] == "RL_ERR_INVALID_ARG" and "scale" in ra.last_error()
+
+
+def test_diagnostics_validate_arguments():
+    lib, d = ra.lib(), ctypes.c_double()
+    r = ctypes.byref
+    assert ra.STATUS[lib.rl_attn_diag_read_bandwidth(None, 1024, 1, r(d), None)] == "RL_ERR_INVALID_ARG"
+    assert ra.STATUS[lib.rl_attn_diag_read_bandwidth(ctypes.c_void_p(FAKE), 1000, 1, r(d), None)] == "RL_ERR_INVALID_ARG"
+    assert ra.STATUS[lib.rl_attn_diag_read_bandwidth(ctypes.c_void_p(FAKE + 4), 1024, 1, r(d), None)] == "RL_ERR_INVALID_ARG"
+    assert ra.STATUS[lib.rl_attn_diag_read_bandwidth(ctypes.c_void_p(FAKE), 1024, 0, r(d), None)] == "RL_ERR_INVALID_ARG"
+    assert ra.STATUS[lib.rl_attn_diag_mfma_bf16(0, r(d), None)] == "RL_ERR_INVALID_ARG"
+    assert ra.STATUS[lib.rl_attn_diag_mfma_bf16((1 << 24) + 1, r(d), None)] == "RL_ERR_INVALID_ARG"
+    assert ra.STATUS[lib.rl_attn_diag_mfma_bf16(10, None, None)] == "RL_ERR_INVALID_ARG"
