@@ -17,6 +17,10 @@ What it computes (the plain definition, evaluated directly in float64):
 * merge   -- the log-sum-exp combination of attention results over disjoint
   key ranges (split-KV partials).
 
+Pages hold bf16 values, or OCP FP8 E4M3 codes with one dequantisation scale
+per KV head (the FP8 key-value cache of the paper's case-study rollout,
+section "Case Study", subsection "Configuration").
+
 The paper names the attention kernels its engines run (section "True-On-Policy
 Alignment") but never writes the operation down; the definition used here is
 textbook scaled dot-product attention (Vaswani et al., 2017) with grouped-query
@@ -25,7 +29,9 @@ head sharing (query head h reads KV head h // (Hq // Hkv)).
 Pins: see tests/test_oracle_pins.py (brute-force dense attention via scipy,
 single-key exactness, uniform-key closed form, page-size/page-order
 invariance, split/merge identity, extend<->decode and causal brute force,
-GQA expansion, scale homogeneity, batch permutation, closed-form golden file).
+GQA expansion, scale homogeneity, batch permutation, closed-form golden file,
+FP8 E4M3 decoding against torch's float8_e4m3fn and the format's closed forms,
+FP8 pages against the same values in bf16, per-KV-head scales).
 Parity with values printed in the paper is unpinned: the paper prints none.
 """
 
@@ -36,5 +42,6 @@ from .attention import (  # noqa: F401
     attend_range,
     decode,
     extend,
+    fp8_e4m3_to_f64,
     merge,
 )

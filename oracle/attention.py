@@ -10,7 +10,11 @@ docstring); the formulas are scaled dot-product attention (Vaswani et al.,
 Conventions (readings where the paper is silent):
 
 * bf16 tensors arrive as ``uint16`` bit patterns and are widened exactly to
-  float64; float arrays are taken as given.
+  float64; float arrays are taken as given. An FP8 KV cache arrives as
+  ``uint8`` OCP E4M3 codes with one dequantisation scale per KV head (the
+  case-study rollout engines serve an FP8 key-value cache, section "Case
+  Study", subsection "Configuration", and its configuration table); the
+  oracle decodes the codes exactly and multiplies by the scale.
 * Query head ``h`` of ``Hq`` reads KV head ``h // (Hq // Hkv)``.
 * Scores are ``scale * (q . k)`` with ``scale`` first rounded to float32 (the
   ABI passes a float32); the log-sum-exp is in natural log and includes the
@@ -40,12 +44,41 @@ def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
     return a.astype(np.float64)
 
 
-def gather_head(pages: np.ndarray, block_row: np.ndarray, length: int, g: int) -> np.ndarray:
+def fp8_e4m3_to_f64(bits: np.ndarray) -> np.ndarray:
+    """Decode OCP FP8 E4M3 codes (uint8) to float64, from the format's definition.
+
+    A code is ``s eeee mmm`` with exponent bias 7: ``e == 0`` encodes the
+    subnormals ``(-1)^s * 2^-6 * m/8``; ``e == 15, m == 7`` encodes NaN (the
+    format has no infinities); every other code is ``(-1)^s * 2^(e-7) * (1 + m/8)``
+    (largest finite magnitude 448).
+    """
+    b = np.asarray(bits, dtype=np.uint8).astype(np.int64)
+    sign = np.where(b & 0x80, -1.0, 1.0)
+    e = (b >> 3) & 0xF
+    m = (b & 0x7).astype(np.float64)
+    normal = np.ldexp(1.0 + m / 8.0, (e - 7).astype(np.int64))
+    sub = np.ldexp(m / 8.0, -6)
+    val = np.where(e == 0, sub, normal)
+    val = np.where((e == 15) & (b & 0x7 == 7), np.nan, val)
+    return sign * val
+
+
+def kv_to_f64(x: np.ndarray) -> np.ndarray:
+    """KV elements to float64: uint8 arrays are FP8 E4M3 codes, anything else goes to bf16_bits_to_f64."""
+    a = np.asarray(x)
+    if a.dtype == np.uint8:
+        return fp8_e4m3_to_f64(a)
+    return bf16_bits_to_f64(a)
+
+
+def gather_head(pages: np.ndarray, block_row: np.ndarray, length: int, g: int, head_scale=None) -> np.ndarray:
     """Rows ``0..length-1`` of KV head ``g`` of one sequence, in logical order.
 
-    ``pages`` is ``[num_pages, P, Hkv, D]``; ``block_row`` is the sequence's
-    block-table row. Token ``t`` comes from page ``block_row[t // P]``, slot
-    ``t % P``. Returns float64 ``[length, D]``.
+    ``pages`` is ``[num_pages, P, Hkv, D]`` (bf16 bit patterns, or FP8 E4M3
+    codes as uint8); ``block_row`` is the sequence's block-table row. Token
+    ``t`` comes from page ``block_row[t // P]``, slot ``t % P``. With
+    ``head_scale`` (one dequantisation scale per KV head) an element stands
+    for its decoded value times ``head_scale[g]``. Returns float64 ``[length, D]``.
     """
     page_size = pages.shape[1]
     d = pages.shape[3]
@@ -53,7 +86,9 @@ def gather_head(pages: np.ndarray, block_row: np.ndarray, length: int, g: int) -
     for t in range(0, length, page_size):
         page = int(block_row[t // page_size])
         take = min(page_size, length - t)
-        out[t:t + take] = bf16_bits_to_f64(pages[page, :take, g, :])
+        out[t:t + take] = kv_to_f64(pages[page, :take, g, :])
+    if head_scale is not None:
+        out *= np.float64(head_scale[g])
     return out
 
 
@@ -94,11 +129,12 @@ def _masked_attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float, li
     return o, lse
 
 
-def decode(q, k_pages, v_pages, block_table, seq_lens, scale):
+def decode(q, k_pages, v_pages, block_table, seq_lens, scale, k_scale=None, v_scale=None):
     """Batched decode: ``out[b, h] = softmax_t(scale q[b,h] . K_b[t, g]) V_b[t, g]``, t < L_b.
 
-    q ``[B, Hq, D]``; k_pages/v_pages ``[num_pages, P, Hkv, D]``;
-    block_table ``[B, max_pages]``; seq_lens ``[B]``.
+    q ``[B, Hq, D]``; k_pages/v_pages ``[num_pages, P, Hkv, D]`` (bf16, or FP8
+    E4M3 codes with per-KV-head dequantisation scales ``k_scale``/``v_scale``
+    of shape ``[Hkv]``); block_table ``[B, max_pages]``; seq_lens ``[B]``.
     Returns ``(out [B, Hq, D], lse [B, Hq])`` float64.
     """
     qf = bf16_bits_to_f64(q)
@@ -110,16 +146,17 @@ def decode(q, k_pages, v_pages, block_table, seq_lens, scale):
     for b in range(b_count):
         length = int(seq_lens[b])
         for g in range(hkv):
-            k = gather_head(k_pages, block_table[b], length, g)
-            v = gather_head(v_pages, block_table[b], length, g)
+            k = gather_head(k_pages, block_table[b], length, g, k_scale)
+            v = gather_head(v_pages, block_table[b], length, g, v_scale)
             o, l = attend(qf[b, g * r:(g + 1) * r], k, v, scale)
             out[b, g * r:(g + 1) * r] = o
             lse[b, g * r:(g + 1) * r] = l
     return out, lse
 
 
-def extend(q, qo_indptr, k_pages, v_pages, block_table, kv_lens, scale, row_block: int = 32):
-    """Causal extend over a paged cache.
+def extend(q, qo_indptr, k_pages, v_pages, block_table, kv_lens, scale, row_block: int = 32, k_scale=None,
+           v_scale=None):
+    """Causal extend over a paged cache (pages and scales as in ``decode``).
 
     q ``[total_q, Hq, D]``; sequence ``b`` owns query rows
     ``qo_indptr[b] .. qo_indptr[b+1]-1`` (n_b of them) and holds ``kv_lens[b]``
@@ -142,8 +179,8 @@ def extend(q, qo_indptr, k_pages, v_pages, block_table, kv_lens, scale, row_bloc
         kv = int(kv_lens[b])
         prefix = kv - n
         for g in range(hkv):
-            k = gather_head(k_pages, block_table[b], kv, g)
-            v = gather_head(v_pages, block_table[b], kv, g)
+            k = gather_head(k_pages, block_table[b], kv, g, k_scale)
+            v = gather_head(v_pages, block_table[b], kv, g, v_scale)
             for i0 in range(0, n, row_block):
                 i1 = min(n, i0 + row_block)
                 rows = qf[q0 + i0:q0 + i1, g * r:(g + 1) * r].reshape(-1, d)   # token-major

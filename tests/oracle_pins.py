@@ -14,7 +14,11 @@ a deliberately broken copy of it in the mutation tests) and raises
   attention;
 * GQA expansion to multi-head attention;
 * scale homogeneity ((2q, scale/2) is bitwise the same problem);
-* batch permutation and shared-versus-private prefix pages.
+* batch permutation and shared-versus-private prefix pages;
+* FP8 E4M3 KV pages: every code against torch's independent float8_e4m3fn
+  conversion and the format's closed forms; with unit scales the result equals
+  the bf16 oracle on the same values bitwise; per-KV-head power-of-two scales
+  equal exactly scaled bf16 pages; arbitrary scales agree with brute force.
 
 The paper prints no attention values, so parity with printed values is
 unpinned; the closed-form golden file in ``tests/golden`` stands in for a
@@ -325,5 +329,103 @@ def pin_golden(orc):
             assert abs(lse[b, h] - want) < 1e-14 * max(1.0, abs(want)), f"{case['name']}: lse[{b},{h}]"
 
 
+def _fp8_values_torch(codes: np.ndarray) -> np.ndarray:
+    """FP8 E4M3 codes -> float64 through torch's float8_e4m3fn (an implementation independent of the oracle)."""
+    import torch
+
+    t = torch.from_numpy(np.ascontiguousarray(codes, dtype=np.uint8)).view(torch.float8_e4m3fn)
+    return t.to(torch.float64).numpy()
+
+
+def _fp8_problem(rng, lens=(21, 40, 9), hq=8, hkv=2, ps=8):
+    """Random FP8 codes (finite only) for K and V, paged; and the same values as bf16 bits."""
+    import torch
+
+    lens = np.array(lens, dtype=np.int32)
+    b_count, lmax = len(lens), int(max(lens))
+    q = to_bf16_bits(rng.standard_normal((b_count, hq, D)))
+    pages = []
+    for _ in range(2):
+        x = torch.from_numpy(rng.standard_normal((b_count, lmax, hkv, D)).astype(np.float32) * 3.0)
+        codes = x.to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+        pages.append(codes)
+    rng_pages = np.random.default_rng(int(rng.integers(1 << 30)))
+    kp, bt = pack_pages(pages[0].astype(np.uint16), lens, ps, rng_pages)      # pack as uint16, keep uint8 values
+    vp = np.full_like(kp, 0x7F)
+    for b in range(b_count):
+        for j in range(-(-int(lens[b]) // ps)):
+            take = min(ps, int(lens[b]) - j * ps)
+            vp[bt[b, j], :take] = pages[1][b, j * ps:j * ps + take]
+    kp = np.where(kp == 0x7FC0, 0x7F, kp).astype(np.uint8)                  # NaN filler -> FP8 NaN code
+    vp = vp.astype(np.uint8)
+    return q, kp, vp, bt, lens
+
+
+def _fp8_as_bf16_bits(codes: np.ndarray, factor=None) -> np.ndarray:
+    """The FP8 values (times an optional per-KV-head power of two) as bf16 bits, via torch (exact)."""
+    vals = _fp8_values_torch(codes)
+    if factor is not None:
+        vals = vals * np.asarray(factor, dtype=np.float64)[None, None, :, None]
+    return to_bf16_bits(vals.astype(np.float32))
+
+
+def pin_fp8_codes(orc):
+    codes = np.arange(256, dtype=np.uint8)
+    mine = orc.fp8_e4m3_to_f64(codes)
+    ref = _fp8_values_torch(codes)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(mine), nan) and nan.sum() == 2, "NaN codes"
+    assert np.array_equal(mine[~nan], ref[~nan]), "FP8 E4M3 decoding differs from torch's float8_e4m3fn"
+    closed = {0x00: 0.0, 0x01: 2.0 ** -9, 0x07: 7 * 2.0 ** -9, 0x08: 2.0 ** -6, 0x38: 1.0, 0x3C: 1.5,
+              0x7E: 448.0, 0x80: -0.0, 0xB8: -1.0, 0xFE: -448.0}
+    for c, want in closed.items():
+        assert mine[c] == want and np.signbit(mine[c]) == np.signbit(want), f"code {c:#04x}"
+
+
+def pin_fp8_equals_bf16(orc, seed=9):
+    rng = np.random.default_rng(seed)
+    q, kp, vp, bt, lens = _fp8_problem(rng)
+    ones = np.ones(2, np.float32)
+    o8, l8 = orc.decode(q, kp, vp, bt, lens, 0.0883883, k_scale=ones, v_scale=ones)
+    ob, lb = orc.decode(q, _fp8_as_bf16_bits(kp), _fp8_as_bf16_bits(vp), bt, lens, 0.0883883)
+    assert np.array_equal(o8, ob) and np.array_equal(l8, lb), "FP8 pages differ from the same values in bf16"
+    qo = np.array([0, 5, 45, 54], np.int32)[: len(lens) + 1]
+    qe = to_bf16_bits(rng.standard_normal((int(qo[-1]), 8, D)))
+    kvl = np.maximum(lens, np.diff(qo))
+    e8, m8 = orc.extend(qe, qo, kp, vp, bt, kvl, 0.1, k_scale=ones, v_scale=ones)
+    eb, mb = orc.extend(qe, qo, _fp8_as_bf16_bits(kp), _fp8_as_bf16_bits(vp), bt, kvl, 0.1)
+    assert np.array_equal(e8, eb) and np.array_equal(m8, mb), "FP8 extend differs from bf16"
+
+
+def pin_fp8_scales(orc, seed=10):
+    rng = np.random.default_rng(seed)
+    q, kp, vp, bt, lens = _fp8_problem(rng, lens=(33, 7), hq=4, hkv=2)
+    ks = np.array([0.25, 4.0], np.float32)
+    vs = np.array([2.0, 0.5], np.float32)
+    o8, l8 = orc.decode(q, kp, vp, bt, lens, 0.07, k_scale=ks, v_scale=vs)
+    ob, lb = orc.decode(q, _fp8_as_bf16_bits(kp, ks), _fp8_as_bf16_bits(vp, vs), bt, lens, 0.07)
+    assert np.array_equal(o8, ob) and np.array_equal(l8, lb), "per-KV-head scales are not applied per head"
+    # arbitrary scales against dense brute force (scipy) on the dequantised values
+    ks = np.array([0.013, 0.71], np.float32)
+    vs = np.array([1.7, 0.0042], np.float32)
+    o8, l8 = orc.decode(q, kp, vp, bt, lens, 0.07, k_scale=ks, v_scale=vs)
+    lmax = int(lens.max())
+    kd = np.zeros((len(lens), lmax, 2, D))
+    vd = np.zeros_like(kd)
+    for b in range(len(lens)):
+        for t in range(int(lens[b])):
+            kd[b, t] = _fp8_values_torch(kp[bt[b, t // 8], t % 8]) * ks[:, None].astype(np.float64)
+            vd[b, t] = _fp8_values_torch(vp[bt[b, t // 8], t % 8]) * vs[:, None].astype(np.float64)
+    qf = from_bits(q)
+    for b in range(len(lens)):
+        for h in range(4):
+            g, l = h // 2, int(lens[b])
+            s = float(np.float32(0.07)) * (kd[b, :l, g] @ qf[b, h])
+            want_o = scipy.special.softmax(s) @ vd[b, :l, g]
+            assert _rel(o8[b, h], want_o) < 1e-12, "FP8 decode vs brute force"
+            assert abs(l8[b, h] - scipy.special.logsumexp(s)) < 1e-12 * max(1.0, abs(l8[b, h]))
+
+
 ALL_PINS = [pin_brute_force, pin_single_key, pin_uniform_keys, pin_page_invariance, pin_split_merge,
-            pin_extend, pin_gqa_expansion, pin_scale_homogeneity, pin_batch_and_sharing, pin_golden]
+            pin_extend, pin_gqa_expansion, pin_scale_homogeneity, pin_batch_and_sharing, pin_golden,
+            pin_fp8_codes, pin_fp8_equals_bf16, pin_fp8_scales]

@@ -28,8 +28,13 @@ MUTANTS = {
     "extend_row_order_head_major": ("limits = np.repeat(prefix + np.arange(i0, i1), r)",
                                     "limits = np.tile(prefix + np.arange(i0, i1), r)"),
     "page_index_modulo": ("page = int(block_row[t // page_size])", "page = int(block_row[(t // page_size) % 2])"),
-    "kv_head_ignored": ("out[t:t + take] = bf16_bits_to_f64(pages[page, :take, g, :])",
-                        "out[t:t + take] = bf16_bits_to_f64(pages[page, :take, 0, :])"),
+    "kv_head_ignored": ("out[t:t + take] = kv_to_f64(pages[page, :take, g, :])",
+                        "out[t:t + take] = kv_to_f64(pages[page, :take, 0, :])"),
+    "fp8_exponent_bias": ("(e - 7).astype(np.int64)", "(e - 8).astype(np.int64)"),
+    "fp8_subnormal_exponent": ("sub = np.ldexp(m / 8.0, -6)", "sub = np.ldexp(m / 8.0, -7)"),
+    "fp8_sign_dropped": ("return sign * val", "return val"),
+    "fp8_scale_ignored": ("out *= np.float64(head_scale[g])", "out *= 1.0"),
+    "fp8_scale_wrong_head": ("out *= np.float64(head_scale[g])", "out *= np.float64(head_scale[0])"),
     "gqa_modulo_mapping": ("o, l = attend(qf[b, g * r:(g + 1) * r], k, v, scale)\n            out[b, g * r:(g + 1) * r] = o\n            lse[b, g * r:(g + 1) * r] = l",
                            "o, l = attend(qf[b, g::hkv], k, v, scale)\n            out[b, g::hkv] = o\n            lse[b, g::hkv] = l"),
     "merge_weight_sign": ("w = np.exp(ls - m)", "w = np.exp(m - ls)"),
