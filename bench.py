@@ -64,6 +64,7 @@ def cpu_baseline(w, tensors, budget_s: float):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_ragged64k_hbm_traffic.json")
+TRAFFIC_FILE_FP8 = os.path.join(ROOT, "profiles", "decode_ragged64k_fp8_hbm_traffic.json")
 CALIB_BYTES = 2 << 30   # bytes read and bytes written by the calibration copy
 
 
@@ -85,17 +86,20 @@ def pmc_workload(kind: str = "ragged"):
     """What the counter runs profile.
 
     ragged: three ragged-64K decode calls, then three copies of CALIB_BYTES (the
-    calibration kernel for FETCH_SIZE / WRITE_SIZE); extend: two multi-turn extend
-    calls; group / group-noshare: three decode calls of the 16x8 trajectory-group
-    batch with prefix sharing on / off, then the same calibration copies."""
+    calibration kernel for FETCH_SIZE / WRITE_SIZE); ragged-fp8: the same with FP8
+    E4M3 pages; extend: two multi-turn extend calls; group / group-noshare: three
+    decode calls of the 16x8 trajectory-group batch with prefix sharing on / off,
+    then the same calibration copies."""
     import torch
 
     from paper_2609_08368_amd import rl_attn as ra
     from paper_2609_08368_amd import workloads as wl
 
     dev = torch.device("cuda:0")
-    w = {"ragged": wl.decode_ragged, "extend": wl.extend_multiturn}.get(kind, wl.decode_group_prefix)()
-    t = wl.materialize(w, dev, poison=False)
+    w = {"ragged": wl.decode_ragged, "ragged-fp8": wl.decode_ragged,
+         "extend": wl.extend_multiturn}.get(kind, wl.decode_group_prefix)()
+    fp8 = kind == "ragged-fp8"
+    t = (wl.materialize_fp8 if fp8 else wl.materialize)(w, dev, poison=False)
     out = torch.empty_like(t["q"])
     if kind == "extend":
         for _ in range(2):
@@ -106,15 +110,21 @@ def pmc_workload(kind: str = "ragged"):
         return
     share = {"prefix_share": kind != "group-noshare"}
     for _ in range(3):
-        ra.decode(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out, **share)
+        if fp8:
+            ra.decode_fp8(t["q"], t["k_pages"], t["v_pages"], t["k_scale"], t["v_scale"], t["block_table"],
+                          t["kv_lens"], t["scale"], out=out)
+        else:
+            ra.decode(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out,
+                      **share)
     src = torch.empty(CALIB_BYTES // 2, dtype=torch.bfloat16, device=dev).fill_(1.0)
     dst = torch.empty_like(src)
     torch.cuda.synchronize()
     for _ in range(3):
         dst.copy_(src)
     torch.cuda.synchronize()
-    print(json.dumps({"pmc_workload": kind, "kv_bytes": w.kv_bytes(unique=True), "logical_kv_bytes": w.kv_bytes(),
-                      "calib_bytes": CALIB_BYTES}), flush=True)
+    per_elem = 0.5 if fp8 else 1.0     # kv_bytes() counts bf16 elements
+    print(json.dumps({"pmc_workload": kind, "kv_bytes": int(w.kv_bytes(unique=True) * per_elem),
+                      "logical_kv_bytes": int(w.kv_bytes() * per_elem), "calib_bytes": CALIB_BYTES}), flush=True)
 
 
 def prefix_study(steps: int = 20):
@@ -170,8 +180,9 @@ def summarize_counters(d: str):
         print(f"{kern[-40:]:40s} {ctr:32s} dispatches {len(vals):3d}  mean {sum(vals) / len(vals):.6g}")
 
 
-def summarize_pmc(fetch_dir: str, write_dir: str):
-    """Turn the FETCH_SIZE and WRITE_SIZE runs into the committed traffic summary."""
+def summarize_pmc(fetch_dir: str, write_dir: str, fp8: bool = False):
+    """Turn the FETCH_SIZE and WRITE_SIZE runs into the committed traffic summary
+    (``fp8``: runs of the ``ragged-fp8`` workload)."""
     import csv
     import glob
 
@@ -199,30 +210,88 @@ def summarize_pmc(fetch_dir: str, write_dir: str):
     dec_fetch = fetch["decode"] * 1024.0 * f_scale
     dec_write = write["decode"] * 1024.0 * w_scale
     w = wl.decode_ragged()
+    algo = w.kv_bytes() // 2 if fp8 else w.kv_bytes()
     res = {
-        "kernel": "decode_mfma_kernel", "workload": "ragged 64K decode batch (B128, Hq96/Hkv8, page 64)",
+        "kernel": "decode_mfma_kernel<true>" if fp8 else "decode_mfma_kernel<false>",
+        "workload": "ragged 64K decode batch (B128, Hq96/Hkv8, page 64)" + (", FP8 E4M3 pages" if fp8 else ", bf16 pages"),
         "source_hash": kernel_source_hash(),
         "fetch_kib_per_dispatch": fetch["decode"], "write_kib_per_dispatch": write["decode"],
         "copy_fetch_kib": fetch["copy"], "copy_write_kib": write["copy"], "calib_bytes": CALIB_BYTES,
         "fetch_scale": f_scale, "write_scale": w_scale,
         "hbm_read_bytes": dec_fetch, "hbm_write_bytes": dec_write, "traffic_bytes": dec_fetch + dec_write,
-        "algorithmic_bytes": w.kv_bytes(),
-        "traffic_over_algorithmic": (dec_fetch + dec_write) / w.kv_bytes(),
+        "algorithmic_bytes": algo,
+        "traffic_over_algorithmic": (dec_fetch + dec_write) / algo,
     }
-    with open(TRAFFIC_FILE, "w") as f:
+    with open(TRAFFIC_FILE_FP8 if fp8 else TRAFFIC_FILE, "w") as f:
         json.dump(res, f, indent=1)
     print(json.dumps(res, indent=1))
 
 
-def traffic_bytes():
+def traffic_bytes(fp8: bool = False):
     """HBM bytes per decode launch from the committed counter summary, or None
     when the summary is missing or the kernel sources changed since it was taken."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(TRAFFIC_FILE_FP8 if fp8 else TRAFFIC_FILE) as f:
             d = json.load(f)
     except (OSError, ValueError):
         return None
     return d["traffic_bytes"] if d.get("source_hash") == kernel_source_hash() else None
+
+
+def fp8_study(steps: int, warmup: int, w_dec, w_ext, bf16_dec_ms: float, bf16_ext_ms: float) -> dict:
+    """Time decode and extend of the same batches with FP8 E4M3 KV pages."""
+    import torch
+
+    from paper_2609_08368_amd import rl_attn as ra
+    from paper_2609_08368_amd import workloads as wl
+
+    dev = torch.device("cuda:0")
+    log("FP8 KV pages: materialising ...")
+    res = {"format": "OCP E4M3 codes, one fp32 dequantisation scale per KV head (amax / 448)"}
+    for name, w in (("decode_ragged", w_dec), ("extend_multiturn", w_ext)):
+        t = wl.materialize_fp8(w, dev, poison=False)
+        out = torch.empty_like(t["q"])
+        if w.kind == "decode":
+            def fn():
+                ra.decode_fp8(t["q"], t["k_pages"], t["v_pages"], t["k_scale"], t["v_scale"], t["block_table"],
+                              t["kv_lens"], t["scale"], out=out)
+        else:
+            def fn():
+                ra.extend_fp8(t["q"], t["qo_indptr"], t["k_pages"], t["v_pages"], t["k_scale"], t["v_scale"],
+                              t["block_table"], t["kv_lens"], t["scale"], out=out)
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        kind = "decode" if w.kind == "decode" else "extend"
+        ra.profile_read(kind)
+        ra.profile_enable(True)
+        stream = torch.cuda.current_stream()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(steps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        ra.profile_enable(False)
+        n_k, kern_ms = ra.profile_read(kind)
+        ms = a.elapsed_time(b) / steps
+        fp8_bytes = w.kv_bytes() // 2          # one byte per element
+        row = {"ms_mean": round(ms, 4), "kernel_ms": round(kern_ms, 4) if n_k else None,
+               "speedup_vs_bf16": round((bf16_dec_ms if kind == "decode" else bf16_ext_ms) / ms, 3)}
+        if kind == "decode":
+            row.update({"kv_bytes": fp8_bytes, "traffic": traffic_bytes(fp8=True),
+                        "kv_GBps": round(fp8_bytes / (ms * 1e-3) / 1e9, 2),
+                        "hbm_frac": round(fp8_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                        "kernel_GBps": round(fp8_bytes / (kern_ms * 1e-3) / 1e9, 2) if n_k else None,
+                        "tokens_per_s": round(w.batch / (ms * 1e-3), 1)})
+        else:
+            row.update({"tflops": round(w.flops() / (ms * 1e-3) / 1e12, 2),
+                        "mfma_frac": round(w.flops() / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)})
+        res[name] = row
+        log(f"FP8 {name}: {row}")
+        del t, out
+        torch.cuda.empty_cache()
+    return res
 
 
 def main():
@@ -232,15 +301,17 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--pmc-workload", nargs="?", const="ragged", choices=["ragged", "extend", "group", "group-noshare"],
+    ap.add_argument("--pmc-workload", nargs="?", const="ragged",
+                    choices=["ragged", "ragged-fp8", "extend", "group", "group-noshare"],
                     help="run only what a counter run profiles")
     ap.add_argument("--summarize-counters", metavar="PMC_DIR", help="per-kernel means of a rocprofv3 --pmc run")
     ap.add_argument("--prefix-study", action="store_true", help="time group-prefix decode with sharing on and off")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the HBM traffic summary from two rocprofv3 --pmc output directories")
+    ap.add_argument("--fp8", action="store_true", help="with --summarize-pmc: runs of --pmc-workload ragged-fp8")
     args = ap.parse_args()
     if args.summarize_pmc:
-        summarize_pmc(*args.summarize_pmc)
+        summarize_pmc(*args.summarize_pmc, fp8=args.fp8)
         return
     if args.pmc_workload:
         pmc_workload(args.pmc_workload)
@@ -387,8 +458,14 @@ def main():
             "algorithmic_bytes": kv_dec,
         },
     }
+    # the same ragged decode and extend batches with FP8 E4M3 KV pages (per-KV-head scales):
+    # reported beside the bf16 step, not part of it
+    del t_grp
+    torch.cuda.empty_cache()
+    result["fp8_kv"] = fp8_study(args.steps, args.warmup, w_dec, w_ext, mean["decode_ragged"],
+                                 mean["extend_multiturn"])
     # measured ceilings on this device, beside the specification peaks
-    del t_grp, t_ext
+    del t_ext
     torch.cuda.empty_cache()
     buf = torch.ones(4 << 30, dtype=torch.uint8, device=dev)
     read_gbps = ra.diag_read_bandwidth(buf, reps=10)

@@ -42,7 +42,7 @@
  * thread-safe. Page ids and lengths read on the device are clamped into the
  * valid ranges, so no input can make a kernel read outside the given buffers;
  * out-of-range values are counted in a device error word that
- * rl_attn_check_device_errors() reports.
+ * rl_attn_check_device_errors() reports (as are invalid FP8 dequantisation scales).
  *
  * Memory: the library owns one workspace per (device, stream), grown with
  * hipMalloc on demand (or ahead of time with rl_attn_reserve_workspace) and
@@ -58,7 +58,9 @@
 extern "C" {
 #endif
 
-enum rl_dtype { RL_BF16 = 1, RL_F32 = 2, RL_I32 = 3 };
+/* RL_FP8_E4M3: one byte per element, the OCP 8-bit E4M3 format (exponent bias
+ * 7, no infinities, 0x7F/0xFF are NaN, largest finite magnitude 448). */
+enum rl_dtype { RL_BF16 = 1, RL_F32 = 2, RL_I32 = 3, RL_FP8_E4M3 = 4 };
 
 enum rl_status {
   RL_OK = 0,
@@ -128,6 +130,34 @@ int rl_attn_extend_ex(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_t
                       const rl_tensor* v_pages, const rl_tensor* block_table, const rl_tensor* kv_lens,
                       float scale, rl_tensor* out, rl_tensor* lse_out, const rl_attn_opts* opts,
                       void* stream);
+
+/* FP8 KV pages (paper: the rollout engine of the case study, section "Case
+ * Study", subsection "Configuration" and its configuration table, serves with
+ * an FP8 key-value cache; section "Low-Precision Training" describes the
+ * "BF16 train, FP8 serve" arrangement). The paper gives no KV cache format,
+ * so the cache here holds E4M3 codes with one fp32 dequantisation scale per
+ * KV head. Key t of head g has the value k_scale[g] * E4M3(k_pages[..]), value
+ * rows v_scale[g] * E4M3(v_pages[..]); the attention is otherwise exactly
+ * rl_attn_decode_ex / rl_attn_extend_ex on those values.
+ *   k_pages, v_pages  [num_pages, P, Hkv, 128] RL_FP8_E4M3 (strides as for bf16,
+ *                     but multiples of 16 elements)
+ *   k_scale, v_scale  [Hkv] f32, device pointers; each entry must be positive
+ *                     and finite (checked on the device: a bad scale is
+ *                     reported by rl_attn_check_device_errors and its head's
+ *                     output is not meaningful)
+ * Codes are converted exactly to bf16 for the matrix products. Pages must
+ * hold no NaN codes (0x7F, 0xFF) in the rows a call reads: the outputs of a
+ * KV head that reads one are unspecified. Everything else (q, out, lse_out, opts, errors) is as for the
+ * bf16 calls. */
+int rl_attn_decode_fp8(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages,
+                       const rl_tensor* k_scale, const rl_tensor* v_scale, const rl_tensor* block_table,
+                       const rl_tensor* seq_lens, float scale, rl_tensor* out, rl_tensor* lse_out,
+                       const rl_attn_opts* opts, void* stream);
+
+int rl_attn_extend_fp8(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor* k_pages,
+                       const rl_tensor* v_pages, const rl_tensor* k_scale, const rl_tensor* v_scale,
+                       const rl_tensor* block_table, const rl_tensor* kv_lens, float scale, rl_tensor* out,
+                       rl_tensor* lse_out, const rl_attn_opts* opts, void* stream);
 
 /* Log-sum-exp merge of partial attention results over disjoint key ranges
  * (the split-KV combine, exposed for testing and for callers that split work

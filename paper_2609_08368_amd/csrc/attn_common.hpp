@@ -103,6 +103,70 @@ __device__ __forceinline__ bf16x8 load_bf16x8(const __bf16* p) {
 
 __device__ __forceinline__ __bf16 bits_to_bf16(u16 b) { return __builtin_bit_cast(__bf16, b); }
 
+// Bytes per stored KV element: bf16, or an FP8 E4M3 code.
+template <bool kFp8>
+constexpr int kv_bytes() { return kFp8 ? 1 : 2; }
+
+// Eight consecutive stored KV elements as loaded from memory: a bf16x8, or
+// eight FP8 E4M3 codes. Kernels that prefetch keep this raw form in flight and
+// convert where the values are used, so a conversion never waits on a load
+// that was issued for a later step.
+template <bool kFp8>
+struct KvRawOf {
+  typedef bf16x8 type;
+};
+template <>
+struct KvRawOf<true> {
+  typedef uint2 type;
+};
+template <bool kFp8>
+using KvRaw = typename KvRawOf<kFp8>::type;
+
+template <bool kFp8>
+__device__ __forceinline__ KvRaw<kFp8> load_kv_raw(const char* p) {
+  return *reinterpret_cast<const KvRaw<kFp8>*>(p);
+}
+
+// Raw elements as a bf16x8 MFMA operand: bf16 as stored; FP8 E4M3 codes
+// converted by the gfx950 packed conversion, two per instruction, which is
+// exact (every E4M3 value, subnormals included, is a bf16 value; the
+// conversion's scale is 1).
+template <bool kFp8>
+__device__ __forceinline__ bf16x8 kv_to_bf16x8(KvRaw<kFp8> w) {
+  if constexpr (!kFp8) {
+    return w;
+  } else {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const bf16x2 a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w.x, 1.0f, false);
+    const bf16x2 b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w.x, 1.0f, true);
+    const bf16x2 c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w.y, 1.0f, false);
+    const bf16x2 d = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w.y, 1.0f, true);
+    return bf16x8{a.x, a.y, b.x, b.y, c.x, c.y, d.x, d.y};
+  }
+}
+
+// Load and convert at once (for loads whose values are used right away).
+template <bool kFp8>
+__device__ __forceinline__ bf16x8 load_kv8(const char* p) {
+  return kv_to_bf16x8<kFp8>(load_kv_raw<kFp8>(p));
+}
+
+// Dequantisation scales of KV head g (1 for bf16 pages); *bad is set when a
+// scale is not positive and finite.
+struct KvScales {
+  float k, v;
+};
+template <bool kFp8, typename KV>
+__device__ __forceinline__ KvScales kv_scales(const KV& kv, int g, int* bad) {
+  if constexpr (!kFp8) {
+    return {1.f, 1.f};
+  } else {
+    const float ks = kv.k_scale[g * kv.ks_s], vs = kv.v_scale[g * kv.vs_s];
+    if (!(ks > 0.f && ks < __builtin_huge_valf()) || !(vs > 0.f && vs < __builtin_huge_valf())) *bad = 1;
+    return {ks, vs};
+  }
+}
+
 // Page id of logical token t, clamped into the pool (a bad id is recorded in
 // *bad). The host guarantees that block-table column strides and indices fit
 // 24 bits, so the index is a single 24-bit multiply.

@@ -306,12 +306,47 @@ __device__ __forceinline__ void for_each_piece(const DecodeArgs& a, int w, F&& f
   }
 }
 
+// A lane's share of one key row of one KV head, as four 8-element chunks of
+// the head dimension: chunk c of lane group grp holds elements d0 = 32 grp +
+// 8 c .. d0 + 7, so a lane's chunks are contiguous (64 bytes of bf16, or 32
+// bytes of FP8 codes: two 16-byte loads rather than four 8-byte ones, which
+// would move half the bytes per load instruction). The scores only need Q and
+// K in the same order, and V is staged into LDS by position. Rows are kept as
+// loaded and converted where they are used.
+template <bool kFp8>
+struct RowPart;
+template <>
+struct RowPart<false> {
+  bf16x8 r[4];
+  __device__ static int d0(int c, int grp) { return 32 * grp + 8 * c; }
+  __device__ void load(const char* row, int grp) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) r[c] = *reinterpret_cast<const bf16x8*>(row + 2 * d0(c, grp));
+  }
+  __device__ bf16x8 chunk(int c) const { return r[c]; }
+};
+template <>
+struct RowPart<true> {
+  uint4 r[2];
+  __device__ static int d0(int c, int grp) { return 32 * grp + 8 * c; }
+  __device__ void load(const char* row, int grp) {
+    r[0] = *reinterpret_cast<const uint4*>(row + 32 * grp);
+    r[1] = *reinterpret_cast<const uint4*>(row + 32 * grp + 16);
+  }
+  __device__ bf16x8 chunk(int c) const {
+    const uint4 w = r[c >> 1];
+    return kv_to_bf16x8<true>((c & 1) ? make_uint2(w.z, w.w) : make_uint2(w.x, w.y));
+  }
+};
+
 // Split-KV decode on MFMA for a packed GQA group of up to 16 query heads.
 // One wave per (private item, KV head, 16-head block). Keys are processed 32
 // at a time: K goes straight from HBM into A-operand registers (each lane
-// loads 4 x 16 contiguous bytes of one key row), V is staged in LDS and read
-// back transposed as the A operand of O^T += V^T P^T. Page ids are loaded one
-// tile ahead of the rows they address.
+// loads its RowPart of one key row), V is staged in LDS and read
+// back transposed as the A operand of O^T += V^T P^T. Rows are fetched one
+// tile ahead (bf16) or two (FP8), and page ids one tile ahead of the rows they
+// address.
+template <bool kFp8>
 __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
   // one V tile per wave (dynamic LDS: the workgroup's waves x 32 keys x 272 B)
   extern __shared__ u16 vs_dyn[];
@@ -336,82 +371,101 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
   const int nrows = min(16, a.R - row0);
   const bool col_ok = col < nrows;
   const int h = g * a.R + row0 + (col_ok ? col : 0);
+  int bad_scale = 0;
+  const KvScales dq = kv_scales<kFp8>(a.kv, g, &bad_scale);
+  const float sl2 = a.scale * dq.k * kLog2e;   // the K dequantisation scale joins the softmax scale
 
   for_each_piece(a, worker, [&](int b, int t_begin, int t_end, int slot) {
   bf16x8 qv[4];
   {
-    const __bf16* qp = (const __bf16*)a.q + (int64_t)b * a.q_sb + (int64_t)h * a.q_sh + grp * 8;
+    const __bf16* qp = (const __bf16*)a.q + (int64_t)b * a.q_sb + (int64_t)h * a.q_sh;
 #pragma unroll
-    for (int c = 0; c < 4; ++c) qv[c] = col_ok ? load_bf16x8(qp + c * 32) : zero_bf16x8();
+    for (int c = 0; c < 4; ++c) qv[c] = col_ok ? load_bf16x8(qp + RowPart<kFp8>::d0(c, grp)) : zero_bf16x8();
   }
 
   f32x4 o[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) o[j] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = kNegInf, l_run = 0.f;
-  const float sl2 = a.scale * kLog2e;
 
   const int* bt_row = a.kv.bt + (int64_t)b * a.kv.bt_sb;
   const uint32_t bt_sj = (uint32_t)a.kv.bt_sj;
-  const __bf16* kbase = (const __bf16*)a.kv.k + (int64_t)g * a.kv.sh + grp * 8;
-  const __bf16* vbase = (const __bf16*)a.kv.v + (int64_t)g * a.kv.v_sh + grp * 8;
+  constexpr int ES = kv_bytes<kFp8>();
+  const char* kbase = (const char*)a.kv.k + ES * (int64_t)g * a.kv.sh;
+  const char* vbase = (const char*)a.kv.v + ES * (int64_t)g * a.kv.v_sh;
   const uint32_t ksp = (uint32_t)a.kv.sp, kss = (uint32_t)a.kv.ss;
   const uint32_t vsp = (uint32_t)a.kv.v_sp, vss = (uint32_t)a.kv.v_ss;
   const int pmask = a.kv.page_size - 1;
   // tiles start at multiples of 32 keys, so a page of >= 32 keys holds a whole tile
   const bool page_holds_tile = a.kv.page_size >= kTile && (t_begin & (kTile - 1)) == 0;
 
-  if (t_begin < t_end) {
-    bf16x8 kc[2][4], vc[2][4];
-    int praw[2];
+  // The two ways of finding a tile's pages are separate code paths, so the
+  // scalar page ids of the first never merge with the vector ones of the other.
+  auto run = [&](auto holds_tag) {
+    constexpr bool kHolds = decltype(holds_tag)::value;
+    // Rows of the next kDepth tiles are in flight while a tile is computed.
+    // FP8 rows are half the bytes, so they go two tiles ahead (the same bytes
+    // and registers in flight as one bf16 tile).
+    constexpr int kDepth = kFp8 ? 2 : 1;
+    typedef RowPart<kFp8> Raw[2];       // rows in flight (key 16 hh + col)
+    Raw kc0, vc0, kc1, vc1;
+    int praw[2];                        // page ids of the next tile to fetch
+    // When a page holds the whole tile its id is the same for the wave and is
+    // read through the scalar unit (the block table is not written while the
+    // kernel runs). Its wait then does not include the vector loads of rows
+    // issued before it, which retire in order.
+    typedef __attribute__((address_space(4))) const int ConstInt;
+    const ConstInt* bt_c = (const ConstInt*)bt_row;
     auto fetch_pages = [&](int t0) {
+      if constexpr (kHolds) {
+        const int t = __builtin_amdgcn_readfirstlane(t0 < t_end ? t0 : t_end - 1);
+        praw[0] = bt_c[__umul24((uint32_t)(t >> a.kv.log2_page), bt_sj)];
+        praw[1] = 0;
+      } else {
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        int t = t0 + (page_holds_tile ? 0 : 16 * hh + col);
-        t = t < t_end ? t : t_end - 1;
-        praw[hh] = (page_holds_tile && hh) ? 0 : bt_row[__umul24((uint32_t)(t >> a.kv.log2_page), bt_sj)];
+        for (int hh = 0; hh < 2; ++hh) {
+          int t = t0 + 16 * hh + col;
+          t = t < t_end ? t : t_end - 1;
+          praw[hh] = bt_row[__umul24((uint32_t)(t >> a.kv.log2_page), bt_sj)];
+        }
       }
     };
-    auto fetch_rows = [&](int t0) {
+    auto fetch_rows = [&](int t0, Raw& kc, Raw& vc) {
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
         int t = t0 + 16 * hh + col;
         t = t < t_end ? t : t_end - 1;
-        int pg = praw[page_holds_tile ? 0 : hh];
+        int pg = praw[kHolds ? 0 : hh];
         if ((unsigned)pg >= (unsigned)a.kv.num_pages) {
           bad = 1;
           pg = pg < 0 ? 0 : a.kv.num_pages - 1;
         }
-        const __bf16* kp = kbase + row_offset((uint32_t)pg, ksp, t & pmask, kss);
-        const __bf16* vp = vbase + row_offset((uint32_t)pg, vsp, t & pmask, vss);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          kc[hh][c] = load_bf16x8(kp + c * 32);
-          vc[hh][c] = load_bf16x8(vp + c * 32);
-        }
+        kc[hh].load(kbase + ES * row_offset((uint32_t)pg, ksp, t & pmask, kss), grp);
+        vc[hh].load(vbase + ES * row_offset((uint32_t)pg, vsp, t & pmask, vss), grp);
       }
     };
-    fetch_pages(t_begin);
-    fetch_rows(t_begin);
-    if (t_begin + kTile < t_end) fetch_pages(t_begin + kTile);
-    for (int t0 = t_begin; t0 < t_end; t0 += kTile) {
+    // one tile of keys [t0, t0 + 32) from the rows in (kc, vc), which then take
+    // the rows kDepth tiles ahead. Prefetches past the piece are clamped to its
+    // last key (in bounds, and never used): unconditional loads keep the number
+    // of loads in flight the same on every path, so each wait covers only the
+    // tile it needs.
+    auto tile = [&](int t0, Raw& kc, Raw& vc) {
       __syncthreads();  // previous tile's V reads are done
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
         for (int c = 0; c < 4; ++c)
-          *reinterpret_cast<bf16x8*>(&vs[16 * hh + col][c * 32 + grp * 8]) = vc[hh][c];
+          *reinterpret_cast<bf16x8*>(&vs[16 * hh + col][RowPart<kFp8>::d0(c, grp)]) = vc[hh].chunk(c);
       f32x4 st[2];
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) st[hh] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int c = 0; c < 4; ++c)
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) st[hh] = mfma_16x16x32(kc[hh][c], qv[c], st[hh]);
-      if (t0 + kTile < t_end) {
-        fetch_rows(t0 + kTile);
-        if (t0 + 2 * kTile < t_end) fetch_pages(t0 + 2 * kTile);
-      }
+        for (int hh = 0; hh < 2; ++hh) st[hh] = mfma_16x16x32(kc[hh].chunk(c), qv[c], st[hh]);
+      const int tn = t0 + kDepth * kTile;
+      fetch_rows(tn, kc, vc);
+      fetch_pages(tn + kTile);
 
       float mt = kNegInf;
 #pragma unroll
@@ -449,16 +503,41 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
         }
         o[j] = mfma_16x16x32(va, pb, o[j]);
       }
+    };
+    fetch_pages(t_begin);
+    fetch_rows(t_begin, kc0, vc0);
+    if constexpr (kDepth == 2) {
+      fetch_pages(t_begin + kTile);
+      fetch_rows(t_begin + kTile, kc1, vc1);
     }
+    fetch_pages(t_begin + kDepth * kTile);
+    if constexpr (kDepth == 1) {
+      for (int t0 = t_begin; t0 < t_end; t0 += kTile) tile(t0, kc0, vc0);
+    } else {
+      // Tiles go in pairs, one per buffer, with no branch between them: the
+      // second tile of the last pair may lie past the piece, where every key is
+      // masked (p = 0, alpha = 1), which leaves o, m and l exactly unchanged.
+      for (int t0 = t_begin; t0 < t_end; t0 += 2 * kTile) {
+        tile(t0, kc0, vc0);
+        tile(t0 + kTile, kc1, vc1);
+      }
+    }
+  };
+  if (t_begin < t_end) {
+    if (page_holds_tile)
+      run(std::true_type{});
+    else
+      run(std::false_type{});
   }
 
   const HeadResult res = finish(m_run, group_sum(l_run));
+  const float inv = res.inv * dq.v;            // the V dequantisation scale
   if (col_ok) {
     if (slot < 0) {
       if (a.out_f32) {
         float* op = (float*)a.out + (int64_t)b * a.out_sb + (int64_t)h * a.out_sh + 4 * grp;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) *reinterpret_cast<f32x4*>(op + 16 * j) = o[j] * res.inv;
+        for (int j = 0; j < 8; ++j) *reinterpret_cast<f32x4*>(op + 16 * j) = o[j] * inv;
       } else {
         typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
         __bf16* op = (__bf16*)a.out + (int64_t)b * a.out_sb + (int64_t)h * a.out_sh + 4 * grp;
@@ -466,7 +545,7 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
         for (int j = 0; j < 8; ++j) {
           bf16x4 w;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) w[i] = (__bf16)(o[j][i] * res.inv);
+          for (int i = 0; i < 4; ++i) w[i] = (__bf16)(o[j][i] * inv);
           *reinterpret_cast<bf16x4*>(op + 16 * j) = w;
         }
       }
@@ -474,27 +553,30 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
     } else {
       float* pp = a.ws.part_o + ((int64_t)slot * a.Hq + h) * kHeadDim + 4 * grp;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) *reinterpret_cast<f32x4*>(pp + 16 * j) = o[j] * res.inv;
+      for (int j = 0; j < 8; ++j) *reinterpret_cast<f32x4*>(pp + 16 * j) = o[j] * inv;
       if (grp == 0) a.ws.part_lse[(int64_t)slot * a.Hq + h] = res.lse;
     }
   }
   });
   if (bad) atomicOr(a.ws.err, kErrPage);
+  if (bad_scale) atomicOr(a.ws.err, kErrScale);
 }
 
 // Single-query decode (one query head per KV head) on the vector ALUs: each
 // 16-lane group takes one key per step (a whole 256-byte row per load), keeps
 // its own online-softmax state, and the four groups are merged at the end.
+template <bool kFp8>
 __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
   const int worker = blockIdx.x / a.Hkv;
   const int g = blockIdx.x - worker * a.Hkv;
-  int bad = 0;
+  int bad = 0, bad_scale = 0;
   const int lane = threadIdx.x;
   const int c16 = lane & 15, grp = lane >> 4;
   const int h = g;  // R == 1
+  const KvScales dq = kv_scales<kFp8>(a.kv, g, &bad_scale);
+  const float sl2 = a.scale * dq.k * kLog2e;
 
   for_each_piece(a, worker, [&](int b, int t_begin, int t_end, int slot) {
-  const float sl2 = a.scale * kLog2e;
   float qf[8];
   {
     const bf16x8 qq = load_bf16x8((const __bf16*)a.q + (int64_t)b * a.q_sb + (int64_t)h * a.q_sh + c16 * 8);
@@ -506,16 +588,17 @@ __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
   for (int i = 0; i < 8; ++i) acc[i] = 0.f;
   const int* bt_row = a.kv.bt + (int64_t)b * a.kv.bt_sb;
   const uint32_t bt_sj = (uint32_t)a.kv.bt_sj;
-  const __bf16* kbase = (const __bf16*)a.kv.k + (int64_t)g * a.kv.sh + c16 * 8;
-  const __bf16* vbase = (const __bf16*)a.kv.v + (int64_t)g * a.kv.v_sh + c16 * 8;
+  constexpr int ES = kv_bytes<kFp8>();
+  const char* kbase = (const char*)a.kv.k + ES * ((int64_t)g * a.kv.sh + c16 * 8);
+  const char* vbase = (const char*)a.kv.v + ES * ((int64_t)g * a.kv.v_sh + c16 * 8);
   for (int t0 = t_begin; t0 < t_end; t0 += 4) {
     const int t = t0 + grp;
     const bool valid = t < t_end;
     const int tt = valid ? t : t_end - 1;
     const uint32_t pg = page_of(bt_row, bt_sj, tt, a.kv.log2_page, a.kv.num_pages, &bad);
     const int slot_t = tt & (a.kv.page_size - 1);
-    const bf16x8 kk = load_bf16x8(kbase + row_offset(pg, (uint32_t)a.kv.sp, slot_t, (uint32_t)a.kv.ss));
-    const bf16x8 vv = load_bf16x8(vbase + row_offset(pg, (uint32_t)a.kv.v_sp, slot_t, (uint32_t)a.kv.v_ss));
+    const bf16x8 kk = load_kv8<kFp8>(kbase + ES * row_offset(pg, (uint32_t)a.kv.sp, slot_t, (uint32_t)a.kv.ss));
+    const bf16x8 vv = load_kv8<kFp8>(vbase + ES * row_offset(pg, (uint32_t)a.kv.v_sp, slot_t, (uint32_t)a.kv.v_ss));
     float d = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) d += qf[i] * (float)kk[i];
@@ -536,28 +619,30 @@ __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
 #pragma unroll
   for (int i = 0; i < 8; ++i) acc[i] = group_sum(acc[i] * w);
   const HeadResult res = finish(M, l_tot);
+  const float inv = res.inv * dq.v;
   if (grp == 0) {
     if (slot < 0) {
       if (a.out_f32) {
         float* op = (float*)a.out + (int64_t)b * a.out_sb + (int64_t)h * a.out_sh + c16 * 8;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) op[i] = acc[i] * res.inv;
+        for (int i = 0; i < 8; ++i) op[i] = acc[i] * inv;
       } else {
         bf16x8 w8;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) w8[i] = (__bf16)(acc[i] * res.inv);
+        for (int i = 0; i < 8; ++i) w8[i] = (__bf16)(acc[i] * inv);
         *reinterpret_cast<bf16x8*>((__bf16*)a.out + (int64_t)b * a.out_sb + (int64_t)h * a.out_sh + c16 * 8) = w8;
       }
       if (a.lse && c16 == 0) a.lse[(int64_t)b * a.lse_sb + (int64_t)h * a.lse_sh] = res.lse;
     } else {
       float* pp = a.ws.part_o + ((int64_t)slot * a.Hq + h) * kHeadDim + c16 * 8;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) pp[i] = acc[i] * res.inv;
+      for (int i = 0; i < 8; ++i) pp[i] = acc[i] * inv;
       if (c16 == 0) a.ws.part_lse[(int64_t)slot * a.Hq + h] = res.lse;
     }
   }
   });
   if (bad) atomicOr(a.ws.err, kErrPage);
+  if (bad_scale) atomicOr(a.ws.err, kErrScale);
 }
 
 // Group-prefix pass: one workgroup per (shared item, KV head) computes the
@@ -566,6 +651,7 @@ __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
 // one partial per member into that member's slot for this split.
 constexpr int kPrefixWaves = 4;         // waves per group-prefix workgroup: 128 member rows
 
+template <bool kFp8>
 __global__ __launch_bounds__(kPrefixWaves * 64, 2) void prefix_kernel(DecodeArgs a) {
   __shared__ TileLds lds;
   // grid-stride over (shared item, KV head): a batch without trajectory groups
@@ -592,18 +678,20 @@ __global__ __launch_bounds__(kPrefixWaves * 64, 2) void prefix_kernel(DecodeArgs
 #pragma unroll
       for (int e = 0; e < 16; ++e) o[jd][e] = 0.f;
     float m_run = kNegInf, l_run = 0.f;
-    int bad = 0;
-    tile_attend<kPrefixWaves, false>(a.kv, a.scale, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g, t0, t1, t1, t1 - 1, qv, lds, o, m_run,
-                l_run, bad);
+    int bad = 0, bad_scale = 0;
+    const KvScales dq = kv_scales<kFp8>(a.kv, g, &bad_scale);
+    tile_attend<kPrefixWaves, false, kFp8>(a.kv, a.scale * dq.k, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g, t0, t1, t1, t1 - 1,
+                                           qv, lds, o, m_run, l_run, bad);
     const HeadResult res = finish(m_run, sum_l32(l_run));
     if (row_ok) {
       const int slot = a.ws.base[b] + split;
       if (slot < a.max_slots) {
-        store_o_row(a.ws.part_o + ((int64_t)slot * a.Hq + head) * kHeadDim, o, res.inv);
+        store_o_row(a.ws.part_o + ((int64_t)slot * a.Hq + head) * kHeadDim, o, res.inv * dq.v);
         if (lane < 32) a.ws.part_lse[(int64_t)slot * a.Hq + head] = res.lse;
       }
     }
     if (bad) atomicOr(a.ws.err, kErrPage);
+    if (bad_scale) atomicOr(a.ws.err, kErrScale);
     __syncthreads();  // the LDS tiles are reused by the next work unit
   }
 }
@@ -698,37 +786,50 @@ __global__ __launch_bounds__(64) void merge_kernel(MergeArgs a) {
   if (a.lse_out && lane == 0) a.lse_out[(int64_t)n * a.lo_sn + (int64_t)h * a.lo_sh] = lse_v;
 }
 
-}  // namespace
-
-hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream, KernelTimer* timer) {
-  plan_decode_kernel<<<1, 1024, 0, stream>>>(a);
+template <bool kFp8>
+void launch_decode_kernels(const DecodeArgs& a, hipStream_t stream, KernelTimer* timer) {
   const unsigned per_item = a.R == 1 ? a.Hkv : a.Hkv * ((a.R + 15) / 16);
-  if (a.group_cap >= 2) prefix_kernel<<<(unsigned)a.prefix_grid, kPrefixWaves * 64, 0, stream>>>(a);
+  if (a.group_cap >= 2) prefix_kernel<kFp8><<<(unsigned)a.prefix_grid, kPrefixWaves * 64, 0, stream>>>(a);
   if (timer) (void)hipEventRecord(timer->start, stream);
   if (a.R == 1) {
-    decode_valu_kernel<<<(unsigned)a.max_workers * per_item, 64, 0, stream>>>(a);
+    decode_valu_kernel<kFp8><<<(unsigned)a.max_workers * per_item, 64, 0, stream>>>(a);
   } else {
     const unsigned nch = per_item / a.item_waves;
     const unsigned grid = (unsigned)((int64_t)a.max_workers * nch);
     const size_t lds = (size_t)a.item_waves * kTile * (kHeadDim + 8) * sizeof(u16);
-    decode_mfma_kernel<<<grid, 64 * a.item_waves, lds, stream>>>(a);
+    decode_mfma_kernel<kFp8><<<grid, 64 * a.item_waves, lds, stream>>>(a);
   }
   if (timer) (void)hipEventRecord(timer->stop, stream);
+}
+
+template <bool kFp8>
+int workers_per_cu_of(int R, int Hkv, int item_waves) {
+  int blocks = 0;
+  if (R == 1) {
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_valu_kernel<kFp8>, 64, 0) != hipSuccess) blocks = 0;
+    return blocks / Hkv > 1 ? blocks / Hkv : 1;
+  }
+  const size_t lds = (size_t)item_waves * kTile * (kHeadDim + 8) * sizeof(u16);
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_mfma_kernel<kFp8>, 64 * item_waves, lds) != hipSuccess)
+    blocks = 0;
+  const int nch = Hkv * ((R + 15) / 16) / item_waves;
+  return blocks / nch > 1 ? blocks / nch : 1;
+}
+
+}  // namespace
+
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream, KernelTimer* timer) {
+  plan_decode_kernel<<<1, 1024, 0, stream>>>(a);
+  if (a.kv.k_scale)
+    launch_decode_kernels<true>(a, stream, timer);
+  else
+    launch_decode_kernels<false>(a, stream, timer);
   combine_kernel<<<(unsigned)(a.B * a.Hq), 64, 0, stream>>>(a);
   return hipGetLastError();
 }
 
-int decode_workers_per_cu(int R, int Hkv, int item_waves) {
-  int blocks = 0;
-  if (R == 1) {
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_valu_kernel, 64, 0) != hipSuccess) blocks = 0;
-    return blocks / Hkv > 1 ? blocks / Hkv : 1;
-  }
-  const size_t lds = (size_t)item_waves * kTile * (kHeadDim + 8) * sizeof(u16);
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_mfma_kernel, 64 * item_waves, lds) != hipSuccess)
-    blocks = 0;
-  const int nch = Hkv * ((R + 15) / 16) / item_waves;
-  return blocks / nch > 1 ? blocks / nch : 1;
+int decode_workers_per_cu(int R, int Hkv, int item_waves, bool fp8) {
+  return fp8 ? workers_per_cu_of<true>(R, Hkv, item_waves) : workers_per_cu_of<false>(R, Hkv, item_waves);
 }
 
 hipError_t launch_merge(const MergeArgs& a, hipStream_t stream) {

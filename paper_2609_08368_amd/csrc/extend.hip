@@ -98,6 +98,7 @@ __global__ __launch_bounds__(1024) void plan_extend_kernel(ExtendArgs a) {
 
 constexpr int kExtWaves = 8;            // waves per extend workgroup: 256 query rows per unit
 
+template <bool kFp8>
 __global__ __launch_bounds__(kExtWaves * 64, 2) void extend_mfma_kernel(ExtendArgs a) {
   __shared__ TileLds lds;
 
@@ -134,15 +135,19 @@ __global__ __launch_bounds__(kExtWaves * 64, 2) void extend_mfma_kernel(ExtendAr
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[jd][e] = 0.f;
   float m_run = kNegInf, l_run = 0.f;
+  int bad_scale = 0;
+  // the K dequantisation scale joins the softmax scale, the V scale the output
+  const KvScales dq = kv_scales<kFp8>(a.kv, g, &bad_scale);
+  const float scale = a.scale * dq.k;
   const int* bt_row = a.kv.bt + (int64_t)b * a.kv.bt_sb;
   if (uniform_pages(a.kv))
-    tile_attend_pp<kExtWaves, true>(a.kv, a.scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run, l_run, bad);
+    tile_attend_pp<kExtWaves, true, kFp8>(a.kv, scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run, l_run, bad);
   else
-    tile_attend_pp<kExtWaves, false>(a.kv, a.scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run, l_run, bad);
+    tile_attend_pp<kExtWaves, false, kFp8>(a.kv, scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run, l_run, bad);
 
   const float l_tot = sum_l32(l_run);
   if (row_ok) {
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const float inv = l_tot > 0.f ? dq.v / l_tot : 0.f;
     if (a.out_f32)
       store_o_row((float*)a.out + qrow * a.out_st + (int64_t)head * a.out_sh, o, inv);
     else
@@ -152,6 +157,7 @@ __global__ __launch_bounds__(kExtWaves * 64, 2) void extend_mfma_kernel(ExtendAr
           l_tot > 0.f ? (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2 : kNegInf;
   }
   if (bad) atomicOr(a.ws.err, kErrPage);
+  if (bad_scale) atomicOr(a.ws.err, kErrScale);
 }
 
 }  // namespace
@@ -160,7 +166,10 @@ hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream, KernelTimer* t
   plan_extend_kernel<<<1, 1024, 0, stream>>>(a);
   const unsigned grid = (unsigned)a.max_items;
   if (timer) (void)hipEventRecord(timer->start, stream);
-  extend_mfma_kernel<<<grid, kExtWaves * 64, 0, stream>>>(a);
+  if (a.kv.k_scale)
+    extend_mfma_kernel<true><<<grid, kExtWaves * 64, 0, stream>>>(a);
+  else
+    extend_mfma_kernel<false><<<grid, kExtWaves * 64, 0, stream>>>(a);
   if (timer) (void)hipEventRecord(timer->stop, stream);
   return hipGetLastError();
 }

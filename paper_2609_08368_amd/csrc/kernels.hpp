@@ -12,6 +12,7 @@ enum DeviceError : int {
   kErrPage = 2,      // a page id outside [0, num_pages) (clamped)
   kErrIndptr = 4,    // qo_indptr not non-decreasing within [0, total_q] (clamped)
   kErrKvShort = 8,   // kv_lens[b] < chunk length (clamped up)
+  kErrScale = 16,    // an FP8 dequantisation scale that is not positive and finite
 };
 
 // Paged KV cache + block table, shared by decode and extend.
@@ -23,6 +24,11 @@ struct PagedKV {
   const int* bt;          // [B, max_pages] int32
   int64_t bt_sb, bt_sj;
   int num_pages, page_size, log2_page, max_pages;
+  // FP8 E4M3 pages: one dequantisation scale per KV head ([Hkv] fp32, strides
+  // in elements); null for bf16 pages
+  const float* k_scale;
+  const float* v_scale;
+  int64_t ks_s, vs_s;
 };
 
 // Workspace carve-up of one decode call. Private keys: sequence b owns
@@ -130,7 +136,7 @@ double diag_mfma_flops(int iters, int cus);
 
 // Workers of the private decode pass that are resident on one CU at a time
 // (from the kernel's occupancy; a worker is one workgroup per wave group).
-int decode_workers_per_cu(int R, int Hkv, int item_waves);
+int decode_workers_per_cu(int R, int Hkv, int item_waves, bool fp8);
 hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream, KernelTimer* timer);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t stream);
 

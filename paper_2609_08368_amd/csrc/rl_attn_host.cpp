@@ -12,6 +12,7 @@
 #include <map>
 #include <mutex>
 #include <string>
+#include <tuple>
 #include <utility>
 #include <vector>
 
@@ -89,6 +90,7 @@ const char* dtype_name(int d) {
     case RL_BF16: return "bf16";
     case RL_F32: return "f32";
     case RL_I32: return "int32";
+    case RL_FP8_E4M3: return "fp8_e4m3";
     default: return "unknown";
   }
 }
@@ -277,27 +279,27 @@ int target_items_for(int64_t Hq, int64_t Hkv, int cus) {
 }
 
 // workers of the private pass resident on one CU (cached per shape)
-int workers_per_cu(int64_t Hq, int64_t Hkv) {
+int workers_per_cu(int64_t Hq, int64_t Hkv, bool fp8) {
   if (env().workers_per_cu > 0) return env().workers_per_cu;
   static std::mutex mu;
-  static std::map<std::pair<int64_t, int64_t>, int> cache;
+  static std::map<std::tuple<int64_t, int64_t, bool>, int> cache;
   std::lock_guard<std::mutex> lk(mu);
-  auto it = cache.find({Hq, Hkv});
+  auto it = cache.find({Hq, Hkv, fp8});
   if (it != cache.end()) return it->second;
   const int R = (int)(Hq / std::max<int64_t>(1, Hkv));
-  const int n = rl::decode_workers_per_cu(R, (int)Hkv, decode_item_waves(Hq, Hkv));
-  cache[{Hq, Hkv}] = n;
+  const int n = rl::decode_workers_per_cu(R, (int)Hkv, decode_item_waves(Hq, Hkv), fp8);
+  cache[{Hq, Hkv, fp8}] = n;
   return n;
 }
 
 DecodeLayout decode_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t max_pages, int64_t P, int split, int cus,
-                           bool prefix_share) {
+                           bool prefix_share, bool fp8) {
   DecodeLayout L{};
   const int64_t R = Hq / std::max<int64_t>(1, Hkv);
   const int64_t max_tokens = max_pages * P;
   const int64_t T = split > 0 ? B * std::max<int64_t>(1, (max_tokens + split - 1) / split)
                               : (int64_t)target_items_for(Hq, Hkv, cus);
-  const int64_t workers = split > 0 ? T : (int64_t)cus * workers_per_cu(Hq, Hkv);
+  const int64_t workers = split > 0 ? T : (int64_t)cus * workers_per_cu(Hq, Hkv, fp8);
   L.max_items = (int)std::min<int64_t>(T + B, INT32_MAX / 2);
   L.max_workers = (int)std::min<int64_t>(std::max<int64_t>(1, workers), INT32_MAX / 64);
   L.max_slots = (int)std::min<int64_t>(L.max_workers + T + 2 * B, INT32_MAX / 2);
@@ -325,12 +327,29 @@ DecodeLayout decode_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t max_pages
   return L;
 }
 
-int fill_paged(const rl_tensor* k, const rl_tensor* v, const rl_tensor* bt, int64_t B, rl::PagedKV* kv) {
+// One dequantisation scale per KV head: [Hkv] f32. The values are checked on
+// the device (positive and finite), where they are read.
+int check_head_scales(const rl_tensor* t, const char* name, int64_t Hkv) {
+  RL_TRY(check_view(t, name, 1));
+  RL_TRY(check_dtype(t, name, RL_F32));
+  if (t->shape[0] != Hkv)
+    return fail(RL_ERR_SHAPE, "%s must have one entry per KV head (%lld, got %lld)", name, (long long)Hkv,
+                (long long)t->shape[0]);
+  if (t->strides[0] < 0 || t->strides[0] > INT32_MAX)
+    return fail(RL_ERR_UNSUPPORTED, "%s: stride must be in [0, 2^31)", name);
+  RL_TRY(check_data(t, name));
+  return RL_OK;
+}
+
+// Paged K/V and block table. kv_dtype is RL_BF16, or RL_FP8_E4M3 with
+// per-KV-head scales k_scale and v_scale (both null for bf16).
+int fill_paged(const rl_tensor* k, const rl_tensor* v, const rl_tensor* bt, int64_t B, int kv_dtype,
+               const rl_tensor* k_scale, const rl_tensor* v_scale, rl::PagedKV* kv) {
   RL_TRY(check_view(k, "k_pages", 4));
   RL_TRY(check_view(v, "v_pages", 4));
   RL_TRY(check_view(bt, "block_table", 2));
-  RL_TRY(check_dtype(k, "k_pages", RL_BF16));
-  RL_TRY(check_dtype(v, "v_pages", RL_BF16));
+  RL_TRY(check_dtype(k, "k_pages", kv_dtype));
+  RL_TRY(check_dtype(v, "v_pages", kv_dtype));
   RL_TRY(check_dtype(bt, "block_table", RL_I32));
   for (int i = 0; i < 4; ++i)
     if (k->shape[i] != v->shape[i]) return fail(RL_ERR_SHAPE, "k_pages and v_pages shapes differ (dim %d)", i);
@@ -371,6 +390,20 @@ int fill_paged(const rl_tensor* k, const rl_tensor* v, const rl_tensor* bt, int6
   while ((1 << lg) < P) ++lg;
   kv->log2_page = lg;
   kv->max_pages = (int)bt->shape[1];
+  kv->k_scale = kv->v_scale = nullptr;
+  kv->ks_s = kv->vs_s = 0;
+  if (kv_dtype == RL_FP8_E4M3) {
+    // FP8 rows are read 16 bytes (16 elements) at a time
+    for (int i = 0; i < 3; ++i)
+      if (k->strides[i] % 16 != 0 || v->strides[i] % 16 != 0)
+        return fail(RL_ERR_UNSUPPORTED, "k_pages/v_pages (FP8): strides must be multiples of 16 elements");
+    RL_TRY(check_head_scales(k_scale, "k_scale", k->shape[2]));
+    RL_TRY(check_head_scales(v_scale, "v_scale", k->shape[2]));
+    kv->k_scale = static_cast<const float*>(k_scale->data);
+    kv->v_scale = static_cast<const float*>(v_scale->data);
+    kv->ks_s = k_scale->strides[0];
+    kv->vs_s = v_scale->strides[0];
+  }
   return RL_OK;
 }
 
@@ -395,7 +428,8 @@ int check_lse(const rl_tensor* lse, int64_t rows, int64_t heads) {
   return RL_OK;
 }
 
-int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages, const rl_tensor* block_table,
+int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages, int kv_dtype,
+                const rl_tensor* k_scale, const rl_tensor* v_scale, const rl_tensor* block_table,
                 const rl_tensor* seq_lens, float scale, rl_tensor* out, rl_tensor* lse_out, const rl_attn_opts* opts,
                 void* stream) {
   Opts o;
@@ -406,7 +440,7 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   RL_TRY(check_rows128(q, "q"));
   const int64_t B = q->shape[0], Hq = q->shape[1];
   rl::DecodeArgs a{};
-  RL_TRY(fill_paged(k_pages, v_pages, block_table, B, &a.kv));
+  RL_TRY(fill_paged(k_pages, v_pages, block_table, B, kv_dtype, k_scale, v_scale, &a.kv));
   const int64_t Hkv = k_pages->shape[2];
   if (Hkv < 1 || Hq < 1 || Hq % Hkv != 0)
     return fail(RL_ERR_SHAPE, "query heads (%lld) must be a positive multiple of KV heads (%lld)", (long long)Hq,
@@ -428,7 +462,7 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   const int cus = device_cus(dev);
   const DecodeLayout lay = decode_layout(B, Hq, Hkv, a.kv.max_pages, a.kv.page_size, o.split_tokens, cus,
-                                         o.prefix_share == RL_PREFIX_AUTO);
+                                         o.prefix_share == RL_PREFIX_AUTO, kv_dtype == RL_FP8_E4M3);
   Workspace* w = nullptr;
   RL_TRY(acquire_ws(st, lay.total, &w));
   char* base = static_cast<char*>(w->ptr);
@@ -503,8 +537,9 @@ size_t extend_ws_bytes(int64_t B, int64_t total_q, int64_t Hkv, int64_t R, int* 
 }
 
 int extend_impl(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor* k_pages, const rl_tensor* v_pages,
-                const rl_tensor* block_table, const rl_tensor* kv_lens, float scale, rl_tensor* out,
-                rl_tensor* lse_out, const rl_attn_opts* opts, void* stream) {
+                int kv_dtype, const rl_tensor* k_scale, const rl_tensor* v_scale, const rl_tensor* block_table,
+                const rl_tensor* kv_lens, float scale, rl_tensor* out, rl_tensor* lse_out, const rl_attn_opts* opts,
+                void* stream) {
   Opts o;
   RL_TRY(read_opts(opts, &o));
   RL_TRY(check_scale(scale));
@@ -521,7 +556,7 @@ int extend_impl(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor*
                 (long long)qo_indptr->shape[0]);
   const int64_t total_q = q->shape[0], Hq = q->shape[1];
   rl::ExtendArgs a{};
-  RL_TRY(fill_paged(k_pages, v_pages, block_table, B, &a.kv));
+  RL_TRY(fill_paged(k_pages, v_pages, block_table, B, kv_dtype, k_scale, v_scale, &a.kv));
   const int64_t Hkv = k_pages->shape[2];
   if (Hkv < 1 || Hq < 1 || Hq % Hkv != 0)
     return fail(RL_ERR_SHAPE, "query heads (%lld) must be a positive multiple of KV heads (%lld)", (long long)Hq,
@@ -586,25 +621,45 @@ extern "C" {
 int rl_attn_decode(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages,
                    const rl_tensor* block_table, const rl_tensor* seq_lens, float scale, rl_tensor* out,
                    void* stream) {
-  return decode_impl(q, k_pages, v_pages, block_table, seq_lens, scale, out, nullptr, nullptr, stream);
+  return decode_impl(q, k_pages, v_pages, RL_BF16, nullptr, nullptr, block_table, seq_lens, scale, out, nullptr,
+                     nullptr, stream);
 }
 
 int rl_attn_decode_ex(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages,
                       const rl_tensor* block_table, const rl_tensor* seq_lens, float scale, rl_tensor* out,
                       rl_tensor* lse_out, const rl_attn_opts* opts, void* stream) {
-  return decode_impl(q, k_pages, v_pages, block_table, seq_lens, scale, out, lse_out, opts, stream);
+  return decode_impl(q, k_pages, v_pages, RL_BF16, nullptr, nullptr, block_table, seq_lens, scale, out, lse_out,
+                     opts, stream);
+}
+
+int rl_attn_decode_fp8(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages,
+                       const rl_tensor* k_scale, const rl_tensor* v_scale, const rl_tensor* block_table,
+                       const rl_tensor* seq_lens, float scale, rl_tensor* out, rl_tensor* lse_out,
+                       const rl_attn_opts* opts, void* stream) {
+  return decode_impl(q, k_pages, v_pages, RL_FP8_E4M3, k_scale, v_scale, block_table, seq_lens, scale, out, lse_out,
+                     opts, stream);
 }
 
 int rl_attn_extend(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor* k_pages,
                    const rl_tensor* v_pages, const rl_tensor* block_table, const rl_tensor* kv_lens, float scale,
                    rl_tensor* out, void* stream) {
-  return extend_impl(q, qo_indptr, k_pages, v_pages, block_table, kv_lens, scale, out, nullptr, nullptr, stream);
+  return extend_impl(q, qo_indptr, k_pages, v_pages, RL_BF16, nullptr, nullptr, block_table, kv_lens, scale, out,
+                     nullptr, nullptr, stream);
 }
 
 int rl_attn_extend_ex(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor* k_pages,
                       const rl_tensor* v_pages, const rl_tensor* block_table, const rl_tensor* kv_lens, float scale,
                       rl_tensor* out, rl_tensor* lse_out, const rl_attn_opts* opts, void* stream) {
-  return extend_impl(q, qo_indptr, k_pages, v_pages, block_table, kv_lens, scale, out, lse_out, opts, stream);
+  return extend_impl(q, qo_indptr, k_pages, v_pages, RL_BF16, nullptr, nullptr, block_table, kv_lens, scale, out,
+                     lse_out, opts, stream);
+}
+
+int rl_attn_extend_fp8(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor* k_pages,
+                       const rl_tensor* v_pages, const rl_tensor* k_scale, const rl_tensor* v_scale,
+                       const rl_tensor* block_table, const rl_tensor* kv_lens, float scale, rl_tensor* out,
+                       rl_tensor* lse_out, const rl_attn_opts* opts, void* stream) {
+  return extend_impl(q, qo_indptr, k_pages, v_pages, RL_FP8_E4M3, k_scale, v_scale, block_table, kv_lens, scale, out,
+                     lse_out, opts, stream);
 }
 
 int rl_attn_merge(const rl_tensor* o_parts, const rl_tensor* lse_parts, const rl_tensor* num_parts, rl_tensor* out,
@@ -680,6 +735,7 @@ int rl_attn_check_device_errors(void* stream) {
     if (word & rl::kErrPage) what += " page-id-out-of-range";
     if (word & rl::kErrIndptr) what += " qo_indptr-invalid";
     if (word & rl::kErrKvShort) what += " kv_lens-shorter-than-chunk";
+    if (word & rl::kErrScale) what += " dequant-scale-invalid";
     return fail(RL_ERR_DEVICE, "device-side input errors (values were clamped):%s", what.c_str());
   }
   return RL_OK;
@@ -695,9 +751,13 @@ size_t rl_attn_decode_workspace_size(int64_t batch, int64_t num_q_heads, int64_t
   if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0) return 0;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess) cus = device_cus(dev);
-  return decode_layout(batch, num_q_heads, num_kv_heads, max_pages, page_size, env().split_tokens, cus,
-                       env().prefix_share == RL_PREFIX_AUTO)
-      .total;
+  // bf16 and FP8 pages may keep different numbers of workers resident: the larger layout
+  size_t total = 0;
+  for (bool fp8 : {false, true})
+    total = std::max(total, decode_layout(batch, num_q_heads, num_kv_heads, max_pages, page_size, env().split_tokens,
+                                          cus, env().prefix_share == RL_PREFIX_AUTO, fp8)
+                                .total);
+  return total;
 }
 
 size_t rl_attn_extend_workspace_size(int64_t batch, int64_t total_q, int64_t num_q_heads, int64_t num_kv_heads,

@@ -65,7 +65,7 @@ __device__ __forceinline__ void load_q_operand(const __bf16* row, bool ok, bf16x
 // workgroup (no mask work for those steps). t_lo must be a multiple of kKeys.
 // Accumulates into o (O^T, 4 blocks of 32 dims), m_run (log2 units) and l_run
 // (this lane's half of the row sum; add lane ^ 32's for the total).
-template <int kWaves, bool kDeep>
+template <int kWaves, bool kDeep, bool kFp8 = false>
 __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, const int* bt_row, int g, int t_lo,
                                             int t_hi, int t_full, int limit, const bf16x8 (&qv)[8], TileLds& lds,
                                             f32x16 (&o)[4], float& m_run, float& l_run, int& bad) {
@@ -79,8 +79,9 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
   constexpr int kStageRows = kKeys / kRowStep;      // key rows each thread stages per step
   const uint32_t bt_sj = (uint32_t)kv.bt_sj;
   const int ld_row = tid >> 4, ld_chunk = (tid & 15) * 8;
-  const __bf16* kbase = (const __bf16*)kv.k + (int64_t)g * kv.sh + ld_chunk;
-  const __bf16* vbase = (const __bf16*)kv.v + (int64_t)g * kv.v_sh + ld_chunk;
+  constexpr int ES = kv_bytes<kFp8>();
+  const char* kbase = (const char*)kv.k + ES * ((int64_t)g * kv.sh + ld_chunk);
+  const char* vbase = (const char*)kv.v + ES * ((int64_t)g * kv.v_sh + ld_chunk);
   const uint32_t ksp = (uint32_t)kv.sp, kss = (uint32_t)kv.ss;
   const uint32_t vsp = (uint32_t)kv.v_sp, vss = (uint32_t)kv.v_ss;
   const int pmask = kv.page_size - 1;
@@ -97,7 +98,7 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
       praw[i] = (page_holds_step && i) ? 0 : bt_row[__umul24((uint32_t)(t >> kv.log2_page), bt_sj)];
     }
   };
-  typedef bf16x8 Rows[kStageRows];
+  typedef KvRaw<kFp8> Rows[kStageRows];      // raw rows in flight, converted when staged
   auto fetch_rows = [&](int t0, Rows& kr, Rows& vr) {
 #pragma unroll
     for (int i = 0; i < kStageRows; ++i) {
@@ -108,15 +109,15 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
         bad = 1;
         pg = pg < 0 ? 0 : kv.num_pages - 1;
       }
-      kr[i] = load_bf16x8(kbase + row_offset((uint32_t)pg, ksp, t & pmask, kss));
-      vr[i] = load_bf16x8(vbase + row_offset((uint32_t)pg, vsp, t & pmask, vss));
+      kr[i] = load_kv_raw<kFp8>(kbase + ES * row_offset((uint32_t)pg, ksp, t & pmask, kss));
+      vr[i] = load_kv_raw<kFp8>(vbase + ES * row_offset((uint32_t)pg, vsp, t & pmask, vss));
     }
   };
   auto stage = [&](int buf, const Rows& kr, const Rows& vr) {
 #pragma unroll
     for (int i = 0; i < kStageRows; ++i) {
-      *reinterpret_cast<bf16x8*>(&lds.ks[buf][ld_row + kRowStep * i][ld_chunk]) = kr[i];
-      *reinterpret_cast<bf16x8*>(&lds.vs[buf][ld_row + kRowStep * i][ld_chunk]) = vr[i];
+      *reinterpret_cast<bf16x8*>(&lds.ks[buf][ld_row + kRowStep * i][ld_chunk]) = kv_to_bf16x8<kFp8>(kr[i]);
+      *reinterpret_cast<bf16x8*>(&lds.vs[buf][ld_row + kRowStep * i][ld_chunk]) = kv_to_bf16x8<kFp8>(vr[i]);
     }
   };
 
@@ -281,7 +282,7 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
 // is formed on the scalar unit, and a thread's in-page row offsets are fixed
 // except for the clamp to the last key in the sequence's final step.
 // Otherwise every thread looks up the page of each row it stages.
-template <int kWaves, bool kUniformPages>
+template <int kWaves, bool kUniformPages, bool kFp8 = false>
 __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, const int* bt_row, int g, int t_lo,
                                                int t_hi, int t_full, int limit, const bf16x8 (&qv)[8], TileLds& lds,
                                                f32x16 (&o)[4], float& m_run, float& l_run, int& bad) {
@@ -295,19 +296,19 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
 
   constexpr int kRowStep = kWaves * 4;
   constexpr int kStageRows = kKeys / kRowStep;
-  typedef bf16x8 Rows[kStageRows];
+  typedef KvRaw<kFp8> Rows[kStageRows];      // raw rows in flight, converted when put into LDS
   const uint32_t bt_sj = (uint32_t)kv.bt_sj;
   const int ld_row = tid >> 4, ld_chunk = (tid & 15) * 8;
   const int pmask = kv.page_size - 1;
   auto put_k = [&](int buf, const Rows& r) {
 #pragma unroll
     for (int i = 0; i < kStageRows; ++i)
-      *reinterpret_cast<bf16x8*>(&lds.ks[buf][ld_row + kRowStep * i][ld_chunk]) = r[i];
+      *reinterpret_cast<bf16x8*>(&lds.ks[buf][ld_row + kRowStep * i][ld_chunk]) = kv_to_bf16x8<kFp8>(r[i]);
   };
   auto put_v = [&](int buf, const Rows& r) {
 #pragma unroll
     for (int i = 0; i < kStageRows; ++i)
-      *reinterpret_cast<bf16x8*>(&lds.vs[buf][ld_row + kRowStep * i][ld_chunk]) = r[i];
+      *reinterpret_cast<bf16x8*>(&lds.vs[buf][ld_row + kRowStep * i][ld_chunk]) = kv_to_bf16x8<kFp8>(r[i]);
   };
   const int tr_row = 4 * kg + ((lane & 15) >> 2);
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
@@ -318,8 +319,9 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
 
   // ---- row fetch, per-row page lookups --------------------------------------
   typedef int Ids[kStageRows];
-  const __bf16* kbase = (const __bf16*)kv.k + (int64_t)g * kv.sh + ld_chunk;
-  const __bf16* vbase = (const __bf16*)kv.v + (int64_t)g * kv.v_sh + ld_chunk;
+  constexpr int ES = kv_bytes<kFp8>();
+  const char* kbase = (const char*)kv.k + ES * ((int64_t)g * kv.sh + ld_chunk);
+  const char* vbase = (const char*)kv.v + ES * ((int64_t)g * kv.v_sh + ld_chunk);
   const uint32_t ksp = (uint32_t)kv.sp, kss = (uint32_t)kv.ss;
   const uint32_t vsp = (uint32_t)kv.v_sp, vss = (uint32_t)kv.v_ss;
   const bool page_holds_step = kv.page_size >= kKeys;
@@ -331,7 +333,7 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
       ids[i] = (page_holds_step && i) ? 0 : bt_row[__umul24((uint32_t)(t >> kv.log2_page), bt_sj)];
     }
   };
-  auto fetch = [&](int t0, const Ids& ids, const __bf16* base, uint32_t sp, uint32_t ss, Rows& r) {
+  auto fetch = [&](int t0, const Ids& ids, const char* base, uint32_t sp, uint32_t ss, Rows& r) {
 #pragma unroll
     for (int i = 0; i < kStageRows; ++i) {
       int t = t0 + ld_row + kRowStep * i;
@@ -341,20 +343,20 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
         bad = 1;
         pg = pg < 0 ? 0 : kv.num_pages - 1;
       }
-      r[i] = load_bf16x8(base + row_offset((uint32_t)pg, sp, t & pmask, ss));
+      r[i] = load_kv_raw<kFp8>(base + ES * row_offset((uint32_t)pg, sp, t & pmask, ss));
     }
   };
 
   // ---- row fetch, one scalar page lookup per step ----------------------------
   typedef __attribute__((address_space(4))) const int ConstInt;
   const ConstInt* bt_c = (const ConstInt*)bt_row;
-  const char* kbase_u = (const char*)((const __bf16*)kv.k + (int64_t)g * kv.sh);
-  const char* vbase_u = (const char*)((const __bf16*)kv.v + (int64_t)g * kv.v_sh);
+  const char* kbase_u = (const char*)kv.k + ES * ((int64_t)g * kv.sh);
+  const char* vbase_u = (const char*)kv.v + ES * ((int64_t)g * kv.v_sh);
   uint32_t koff[kStageRows], voff[kStageRows];        // byte offsets of this thread's rows in a step
 #pragma unroll
   for (int i = 0; i < kStageRows; ++i) {
-    koff[i] = 2u * (ld_chunk + (uint32_t)(ld_row + kRowStep * i) * kss);
-    voff[i] = 2u * (ld_chunk + (uint32_t)(ld_row + kRowStep * i) * vss);
+    koff[i] = ES * (ld_chunk + (uint32_t)(ld_row + kRowStep * i) * kss);
+    voff[i] = ES * (ld_chunk + (uint32_t)(ld_row + kRowStep * i) * vss);
   }
   auto page_id = [&](int t0) -> int {
     const int t = t0 < t_last ? t0 : t_last;
@@ -368,16 +370,16 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
   auto fetch_u = [&](int t0, int pg, const char* base, int64_t sp, uint32_t ss, const uint32_t (&off)[kStageRows],
                      Rows& r) {
     const int tc = t0 < t_last ? t0 : t_last;
-    const char* pb = base + 2 * ((int64_t)pg * sp) + 2u * ((uint32_t)(tc & pmask) * ss);
+    const char* pb = base + ES * ((int64_t)pg * sp) + ES * ((uint32_t)(tc & pmask) * ss);
     if (tc + kKeys <= t_hi) {
 #pragma unroll
-      for (int i = 0; i < kStageRows; ++i) r[i] = *reinterpret_cast<const bf16x8*>(pb + off[i]);
+      for (int i = 0; i < kStageRows; ++i) r[i] = load_kv_raw<kFp8>(pb + off[i]);
     } else {
       const int last = t_hi - 1 - tc;
 #pragma unroll
       for (int i = 0; i < kStageRows; ++i) {
         const int rr = min(ld_row + kRowStep * i, last);
-        r[i] = *reinterpret_cast<const bf16x8*>(pb + 2u * (ld_chunk + (uint32_t)rr * ss));
+        r[i] = load_kv_raw<kFp8>(pb + ES * (ld_chunk + (uint32_t)rr * ss));
       }
     }
   };

@@ -21,7 +21,7 @@ LIB_PATH = os.environ.get("RL_ATTN_LIB", os.path.join(_PKG, "librlattn.so"))
 INCLUDE = os.path.join(os.path.dirname(_PKG), "include")
 HEADER = os.path.join(INCLUDE, "rl_attn.h")
 
-RL_BF16, RL_F32, RL_I32 = 1, 2, 3
+RL_BF16, RL_F32, RL_I32, RL_FP8_E4M3 = 1, 2, 3, 4
 RL_PREFIX_AUTO, RL_PREFIX_OFF = 0, 1
 STATUS = {
     0: "RL_OK", -1: "RL_ERR_INVALID_ARG", -2: "RL_ERR_SHAPE", -3: "RL_ERR_DTYPE", -4: "RL_ERR_UNSUPPORTED",
@@ -63,6 +63,8 @@ def lib() -> ctypes.CDLL:
         L.rl_attn_extend.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, vp]
         L.rl_attn_decode_ex.argtypes = [P, P, P, P, P, ctypes.c_float, P, P, ctypes.POINTER(RlOpts), vp]
         L.rl_attn_extend_ex.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, P, ctypes.POINTER(RlOpts), vp]
+        L.rl_attn_decode_fp8.argtypes = [P, P, P, P, P, P, P, ctypes.c_float, P, P, ctypes.POINTER(RlOpts), vp]
+        L.rl_attn_extend_fp8.argtypes = [P, P, P, P, P, P, P, P, ctypes.c_float, P, P, ctypes.POINTER(RlOpts), vp]
         L.rl_attn_merge.argtypes = [P, P, P, P, P, vp]
         L.rl_attn_last_error.restype = ctypes.c_char_p
         L.rl_attn_check_device_errors.argtypes = [vp]
@@ -78,7 +80,7 @@ def lib() -> ctypes.CDLL:
         L.rl_attn_diag_read_bandwidth.argtypes = [vp, ctypes.c_int64, ctypes.c_int32, dp, vp]
         L.rl_attn_diag_mfma_bf16.argtypes = [ctypes.c_int64, dp, vp]
         for name in ("rl_attn_decode", "rl_attn_extend", "rl_attn_decode_ex", "rl_attn_extend_ex",
-                     "rl_attn_merge", "rl_attn_check_device_errors", "rl_attn_reserve_workspace",
+                     "rl_attn_decode_fp8", "rl_attn_extend_fp8", "rl_attn_merge", "rl_attn_check_device_errors", "rl_attn_reserve_workspace",
                      "rl_attn_profile_enable", "rl_attn_profile_read", "rl_attn_diag_read_bandwidth",
                      "rl_attn_diag_mfma_bf16"):
             getattr(L, name).restype = ctypes.c_int
@@ -106,7 +108,8 @@ def _check(rc: int):
         raise RlAttnError(rc, last_error())
 
 
-_DTYPES = {torch.bfloat16: RL_BF16, torch.float32: RL_F32, torch.int32: RL_I32}
+_DTYPES = {torch.bfloat16: RL_BF16, torch.float32: RL_F32, torch.int32: RL_I32,
+           torch.float8_e4m3fn: RL_FP8_E4M3}
 
 
 def view(t: Optional[torch.Tensor]):
@@ -185,6 +188,32 @@ def extend_plain(q, qo_indptr, k_pages, v_pages, block_table, kv_lens, scale, ou
     _check(lib().rl_attn_extend(_ref(view(q)), _ref(view(qo_indptr)), _ref(view(k_pages)), _ref(view(v_pages)),
                                 _ref(view(block_table)), _ref(view(kv_lens)), ctypes.c_float(scale),
                                 _ref(view(out)), _stream(stream)))
+    return out
+
+
+def decode_fp8(q, k_pages, v_pages, k_scale, v_scale, block_table, seq_lens, scale, out=None, lse=None, *,
+               split_tokens=0, prefix_share=True, validate=False, stream=None):
+    """``rl_attn_decode_fp8``: pages are ``torch.float8_e4m3fn``, scales ``[Hkv]`` float32."""
+    if out is None:
+        out = torch.empty_like(q)
+    o = _opts(split_tokens, prefix_share, validate)
+    _check(lib().rl_attn_decode_fp8(_ref(view(q)), _ref(view(k_pages)), _ref(view(v_pages)), _ref(view(k_scale)),
+                                    _ref(view(v_scale)), _ref(view(block_table)), _ref(view(seq_lens)),
+                                    ctypes.c_float(scale), _ref(view(out)), _ref(view(lse)), ctypes.byref(o),
+                                    _stream(stream)))
+    return out
+
+
+def extend_fp8(q, qo_indptr, k_pages, v_pages, k_scale, v_scale, block_table, kv_lens, scale, out=None, lse=None,
+               *, validate=False, stream=None):
+    """``rl_attn_extend_fp8``: pages are ``torch.float8_e4m3fn``, scales ``[Hkv]`` float32."""
+    if out is None:
+        out = torch.empty_like(q)
+    o = _opts(0, True, validate)
+    _check(lib().rl_attn_extend_fp8(_ref(view(q)), _ref(view(qo_indptr)), _ref(view(k_pages)), _ref(view(v_pages)),
+                                    _ref(view(k_scale)), _ref(view(v_scale)), _ref(view(block_table)),
+                                    _ref(view(kv_lens)), ctypes.c_float(scale), _ref(view(out)), _ref(view(lse)),
+                                    ctypes.byref(o), _stream(stream)))
     return out
 
 

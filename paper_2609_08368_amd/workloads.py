@@ -269,6 +269,43 @@ def materialize(w: Paged, device="cpu", poison: bool = True, chunk_pages: int = 
     return out
 
 
+FP8_E4M3_MAX = 448.0
+
+
+def materialize_fp8(w: Paged, device="cpu", poison: bool = True, chunk_pages: int = 2048):
+    """Build a workload with FP8 E4M3 KV pages and per-KV-head scales.
+
+    The bf16 pages of ``materialize`` (same seed, same values) are divided by
+    a per-KV-head scale, amax over that head's pool / 448 (computed in float32),
+    and cast to ``torch.float8_e4m3fn`` (torch's round-to-nearest-even cast);
+    the returned ``k_scale`` / ``v_scale`` are those ``[Hkv]`` float32 scales.
+    Poisoned rows hold the NaN code 0x7F. The bf16 pages are not returned.
+    """
+    import torch
+
+    t = materialize(w, device, poison=False, chunk_pages=chunk_pages)
+    for name in ("k_pages", "v_pages"):
+        src = t.pop(name)
+        amax = torch.zeros(w.hkv, device=src.device, dtype=torch.float32)
+        for p0 in range(0, w.num_pages, chunk_pages):
+            blk = src[p0:p0 + chunk_pages].float().abs()
+            amax = torch.maximum(amax, blk.amax(dim=(0, 1, 3)))
+            del blk
+        scale = torch.where(amax > 0, amax / FP8_E4M3_MAX, torch.ones_like(amax))
+        dst = torch.empty(src.shape, device=src.device, dtype=torch.float8_e4m3fn)
+        inv = scale.view(1, 1, -1, 1)
+        for p0 in range(0, w.num_pages, chunk_pages):
+            x = src[p0:p0 + chunk_pages].float() / inv
+            dst[p0:p0 + chunk_pages] = x.clamp_(-FP8_E4M3_MAX, FP8_E4M3_MAX).to(torch.float8_e4m3fn)
+            del x
+        del src
+        t[name] = dst
+        t[name.replace("pages", "scale")] = scale
+    if poison:
+        poison_pages(w, t["k_pages"].view(torch.uint8), t["v_pages"].view(torch.uint8), fill=0x7F)
+    return t
+
+
 def referenced_pages(w: Paged) -> np.ndarray:
     ids = set()
     for b in range(w.batch):
@@ -277,15 +314,16 @@ def referenced_pages(w: Paged) -> np.ndarray:
     return np.array(sorted(ids), dtype=np.int64)
 
 
-def poison_pages(w: Paged, k_pages, v_pages):
-    """Fill unreferenced pages and the unused tail slots of last pages with NaN."""
+def poison_pages(w: Paged, k_pages, v_pages, fill=float("nan")):
+    """Fill unreferenced pages and the unused tail slots of last pages with NaN
+    (``fill``: the value written, e.g. the E4M3 NaN code on a uint8 view)."""
     import torch
 
     dev = k_pages.device
     used = np.zeros(w.num_pages, dtype=bool)
     used[referenced_pages(w)] = True
     unused = torch.from_numpy(np.nonzero(~used)[0]).to(dev)
-    nan = float("nan")
+    nan = fill
     if unused.numel():
         k_pages.index_fill_(0, unused, nan)
         v_pages.index_fill_(0, unused, nan)
@@ -318,7 +356,7 @@ def compact_subset(w: Paged, tensors: dict, rows):
     Used to check sampled sequences of full-size workloads against the oracle
     without copying the whole pool: the selected sequences' pages are copied
     (in block-table order) into a small pool and the block table is rewritten.
-    Returns a dict of numpy arrays (bf16 as uint16 bits).
+    Returns a dict of numpy arrays (bf16 as uint16 bits, FP8 E4M3 as uint8 codes).
     """
     import torch
 
@@ -341,8 +379,13 @@ def compact_subset(w: Paged, tensors: dict, rows):
     for i, r in enumerate(table):
         bt[i, :len(r)] = r
     ids = torch.tensor(page_ids if page_ids else [0], dtype=torch.long, device=tensors["k_pages"].device)
-    k = to_numpy_bits(tensors["k_pages"].index_select(0, ids))
-    v = to_numpy_bits(tensors["v_pages"].index_select(0, ids))
+    def page_bits(t):
+        if t.dtype == torch.float8_e4m3fn:
+            return t.view(torch.uint8).index_select(0, ids).cpu().numpy()
+        return to_numpy_bits(t.index_select(0, ids))
+
+    k = page_bits(tensors["k_pages"])
+    v = page_bits(tensors["v_pages"])
     res = {"k_pages": k, "v_pages": v, "block_table": bt,
            "kv_lens": w.kv_lens[rows].copy(), "q_lens": w.q_lens[rows].copy()}
     if w.kind == "decode":

@@ -52,12 +52,21 @@ def poison_like(t: torch.Tensor) -> torch.Tensor:
     return t.fill_(float("nan"))
 
 
+def is_fp8(tensors: dict) -> bool:
+    return "k_scale" in tensors
+
+
 def run_decode(w: wl.Paged, tensors: dict, out_dtype=torch.bfloat16, **opts):
+    """The bf16 entry point, or the FP8 one for tensors from ``materialize_fp8``."""
     q = tensors["q"]
     out = poison_like(torch.empty(q.shape, dtype=out_dtype, device=q.device))
     lse = poison_like(torch.empty(q.shape[:2], dtype=torch.float32, device=q.device))
-    ra.decode(q, tensors["k_pages"], tensors["v_pages"], tensors["block_table"], tensors["kv_lens"],
-              tensors["scale"], out=out, lse=lse, **opts)
+    if is_fp8(tensors):
+        ra.decode_fp8(q, tensors["k_pages"], tensors["v_pages"], tensors["k_scale"], tensors["v_scale"],
+                      tensors["block_table"], tensors["kv_lens"], tensors["scale"], out=out, lse=lse, **opts)
+    else:
+        ra.decode(q, tensors["k_pages"], tensors["v_pages"], tensors["block_table"], tensors["kv_lens"],
+                  tensors["scale"], out=out, lse=lse, **opts)
     torch.cuda.synchronize()
     return out, lse
 
@@ -66,17 +75,29 @@ def run_extend(w: wl.Paged, tensors: dict, out_dtype=torch.bfloat16, **opts):
     q = tensors["q"]
     out = poison_like(torch.empty(q.shape, dtype=out_dtype, device=q.device))
     lse = poison_like(torch.empty(q.shape[:2], dtype=torch.float32, device=q.device))
-    ra.extend(q, tensors["qo_indptr"], tensors["k_pages"], tensors["v_pages"], tensors["block_table"],
-              tensors["kv_lens"], tensors["scale"], out=out, lse=lse, **opts)
+    if is_fp8(tensors):
+        ra.extend_fp8(q, tensors["qo_indptr"], tensors["k_pages"], tensors["v_pages"], tensors["k_scale"],
+                      tensors["v_scale"], tensors["block_table"], tensors["kv_lens"], tensors["scale"], out=out,
+                      lse=lse, **opts)
+    else:
+        ra.extend(q, tensors["qo_indptr"], tensors["k_pages"], tensors["v_pages"], tensors["block_table"],
+                  tensors["kv_lens"], tensors["scale"], out=out, lse=lse, **opts)
     torch.cuda.synchronize()
     return out, lse
+
+
+def host_scales(tensors: dict) -> dict:
+    """Per-KV-head dequantisation scales as float64 host arrays (FP8 workloads), else {}."""
+    if not is_fp8(tensors):
+        return {}
+    return {k: tensors[k].cpu().numpy().astype(np.float64) for k in ("k_scale", "v_scale")}
 
 
 def oracle_decode_rows(w: wl.Paged, tensors: dict, rows):
     """Oracle decode of the sequences ``rows`` (compacted host copy of their pages)."""
     sub = wl.compact_subset(w, tensors, rows)
     return oracle.decode(sub["q"], sub["k_pages"], sub["v_pages"], sub["block_table"], sub["kv_lens"],
-                         tensors["scale"])
+                         tensors["scale"], **host_scales(tensors))
 
 
 def oracle_extend_rows(w: wl.Paged, tensors: dict, seq: int, chunk_rows):
@@ -87,17 +108,26 @@ def oracle_extend_rows(w: wl.Paged, tensors: dict, seq: int, chunk_rows):
     outs, lses = [], []
     for i in chunk_rows:
         o, l = oracle.decode(sub["q"][i:i + 1], sub["k_pages"], sub["v_pages"], sub["block_table"],
-                             np.array([p + i + 1]), tensors["scale"])
+                             np.array([p + i + 1]), tensors["scale"], **host_scales(tensors))
         outs.append(o[0])
         lses.append(l[0])
     return np.stack(outs), np.stack(lses)
 
 
+def to_host(v: torch.Tensor) -> np.ndarray:
+    """bf16 -> uint16 bits, FP8 E4M3 -> uint8 codes, anything else as is."""
+    if v.dtype == torch.bfloat16:
+        return wl.to_numpy_bits(v)
+    if v.dtype == torch.float8_e4m3fn:
+        return v.view(torch.uint8).cpu().numpy()
+    return v.cpu().numpy()
+
+
 def oracle_full(w: wl.Paged, tensors: dict):
-    host = {k: (wl.to_numpy_bits(v) if v.dtype == torch.bfloat16 else v.cpu().numpy())
-            for k, v in tensors.items() if isinstance(v, torch.Tensor)}
+    host = {k: to_host(v) for k, v in tensors.items() if isinstance(v, torch.Tensor) and not k.endswith("_scale")}
+    sc = host_scales(tensors)
     if w.kind == "decode":
         return oracle.decode(host["q"], host["k_pages"], host["v_pages"], host["block_table"], host["kv_lens"],
-                             tensors["scale"])
+                             tensors["scale"], **sc)
     return oracle.extend(host["q"], host["qo_indptr"], host["k_pages"], host["v_pages"], host["block_table"],
-                         host["kv_lens"], tensors["scale"])
+                         host["kv_lens"], tensors["scale"], **sc)

@@ -167,3 +167,57 @@ def test_diagnostics_validate_arguments():
     assert ra.STATUS[lib.rl_attn_diag_mfma_bf16(0, r(d), None)] == "RL_ERR_INVALID_ARG"
     assert ra.STATUS[lib.rl_attn_diag_mfma_bf16((1 << 24) + 1, r(d), None)] == "RL_ERR_INVALID_ARG"
     assert ra.STATUS[lib.rl_attn_diag_mfma_bf16(10, None, None)] == "RL_ERR_INVALID_ARG"
+
+
+def fp8_decode_args(Hkv=2):
+    a = decode_args(Hkv=Hkv)
+    a["k"] = fake([10, 16, Hkv, 128], ra.RL_FP8_E4M3)
+    a["v"] = fake([10, 16, Hkv, 128], ra.RL_FP8_E4M3)
+    a["ks"] = fake([Hkv], ra.RL_F32)
+    a["vs"] = fake([Hkv], ra.RL_F32)
+    return a
+
+
+def call_decode_fp8(a):
+    r = ctypes.byref
+    opt = lambda x: r(x) if x is not None else None
+    return ra.lib().rl_attn_decode_fp8(r(a["q"]), r(a["k"]), r(a["v"]), opt(a["ks"]), opt(a["vs"]), r(a["bt"]),
+                                       r(a["lens"]), ctypes.c_float(0.088), r(a["out"]), None, None, None)
+
+
+@pytest.mark.parametrize("mutate,code,needle", [
+    (lambda a: a.update(k=fake([10, 16, 2, 128], ra.RL_BF16)) or a, "RL_ERR_DTYPE", "k_pages must be fp8_e4m3"),
+    (lambda a: a.update(v=fake([10, 16, 2, 128], ra.RL_BF16)) or a, "RL_ERR_DTYPE", "v_pages must be fp8_e4m3"),
+    (lambda a: a.update(ks=None) or a, "RL_ERR_INVALID_ARG", "k_scale is NULL"),
+    (lambda a: a.update(vs=fake([3], ra.RL_F32)) or a, "RL_ERR_SHAPE", "v_scale must have one entry per KV head"),
+    (lambda a: a.update(ks=fake([2], ra.RL_BF16)) or a, "RL_ERR_DTYPE", "k_scale must be f32"),
+    (lambda a: a.update(ks=fake([2, 1], ra.RL_F32)) or a, "RL_ERR_SHAPE", "k_scale must have 1"),
+    (lambda a: a.update(vs=fake([2], ra.RL_F32, ptr=0)) or a, "RL_ERR_INVALID_ARG", "v_scale.data"),
+])
+def test_fp8_validation(mutate, code, needle):
+    rc = call_decode_fp8(mutate(fp8_decode_args()))
+    assert ra.STATUS[rc] == code, ra.last_error()
+    assert needle in ra.last_error(), ra.last_error()
+
+
+def test_fp8_pages_rejected_by_bf16_calls():
+    a = fp8_decode_args()
+    assert ra.STATUS[call_decode(a)] == "RL_ERR_DTYPE" and "k_pages must be bf16" in ra.last_error()
+
+
+def test_fp8_extend_validation():
+    r = ctypes.byref
+    B = 3
+    q = fake([10, 8, 128], ra.RL_BF16)
+    k = fake([20, 16, 2, 128], ra.RL_FP8_E4M3)
+    bt = fake([B, 4], ra.RL_I32)
+    kv = fake([B], ra.RL_I32)
+    out = fake([10, 8, 128], ra.RL_BF16)
+    indptr = fake([B + 1], ra.RL_I32)
+    ks = fake([2], ra.RL_F32)
+    rc = ra.lib().rl_attn_extend_fp8(r(q), r(indptr), r(k), r(k), r(ks), r(fake([1], ra.RL_F32)), r(bt), r(kv),
+                                     ctypes.c_float(1.0), r(out), None, None, None)
+    assert ra.STATUS[rc] == "RL_ERR_SHAPE" and "v_scale" in ra.last_error()
+    rc = ra.lib().rl_attn_extend_fp8(r(q), r(indptr), r(fake([20, 16, 2, 128], ra.RL_BF16)), r(k), r(ks), r(ks),
+                                     r(bt), r(kv), ctypes.c_float(1.0), r(out), None, None, None)
+    assert ra.STATUS[rc] == "RL_ERR_DTYPE"
