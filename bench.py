@@ -294,6 +294,36 @@ def fp8_study(steps: int, warmup: int, w_dec, w_ext, bf16_dec_ms: float, bf16_ex
     return res
 
 
+def deterministic_study(steps: int, warmup: int, w, t, split_ms: float) -> dict:
+    """Time the batch-invariant decode (one extend row per sequence, no key split)."""
+    import torch
+
+    from paper_2609_08368_amd import rl_attn as ra
+
+    out = torch.empty_like(t["q"])
+
+    def fn():
+        ra.decode(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out,
+                  deterministic=True)
+
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(steps):
+        fn()
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    gbps = w.kv_bytes() / (ms * 1e-3) / 1e9
+    res = {"workload": "ragged 64K decode batch, bf16 pages", "ms_mean": round(ms, 4), "kv_GBps": round(gbps, 2),
+           "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4), "slowdown_vs_split_kv": round(ms / split_ms, 3)}
+    log(f"deterministic decode: {res}")
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -462,6 +492,8 @@ def main():
     # reported beside the bf16 step, not part of it
     del t_grp
     torch.cuda.empty_cache()
+    result["deterministic_decode"] = deterministic_study(args.steps, args.warmup, w_dec, t_dec,
+                                                         mean["decode_ragged"])
     result["fp8_kv"] = fp8_study(args.steps, args.warmup, w_dec, w_ext, mean["decode_ragged"],
                                  mean["extend_multiturn"])
     # measured ceilings on this device, beside the specification peaks

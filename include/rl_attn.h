@@ -92,8 +92,24 @@ typedef struct {
                             (RL_ERR_INVALID_ARG if not)                          */
   int32_t prefix_share;  /* enum rl_prefix_mode: read group-shared prefix pages once
                             (AUTO) or treat every sequence independently (OFF)     */
-  int32_t validate;      /* 1: also check every referenced page id on the device   */
-  int32_t reserved[5];   /* must be zero                                          */
+  int32_t validate;      /* accepted for compatibility, no effect: every page id a
+                            kernel reads is range-checked on every call           */
+  int32_t deterministic; /* decode: 1 = batch-invariant and equal to extend. Each
+                            sequence is computed by the extend kernel as one query
+                            row, with no split of its keys, so its out and lse do
+                            not depend on the other sequences of the batch (their
+                            number, order or lengths) and are bitwise equal to
+                            rl_attn_extend_ex of that token (paper: section
+                            "True-On-Policy Alignment" asks for prefill and decode
+                            paths that agree bitwise, and for batch invariance).
+                            Slower on long contexts (no key split). Extend rows
+                            are always invariant in this sense: a row's result
+                            does not depend on the other rows of its chunk, the
+                            chunk's length or the batch, so a prefill of a whole
+                            chunk and its tokens appended one at a time agree
+                            bitwise. 0 = default split-KV decode (results depend
+                            on the batch within the stated tolerance)            */
+  int32_t reserved[4];   /* must be zero                                          */
 } rl_attn_opts;
 
 /* Batched decode (paper: batched generation by the rollout engines).

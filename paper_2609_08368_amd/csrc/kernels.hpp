@@ -75,7 +75,6 @@ struct DecodeArgs {
   int group_cap;          // members per sub-group (128 query rows / R), 0 = no prefix sharing
   int prefix_grid;        // workgroups of the group-prefix pass (grid-stride over its work)
   int item_waves;         // waves per decode workgroup: a divisor of Hkv * ceil(R / 16), at most 8
-  int validate;
   DecodePlanWs ws;
 };
 
@@ -103,7 +102,10 @@ struct ExtendArgs {
   float* lse;
   int64_t lse_st, lse_sh;
   int max_items;
-  int validate;
+  // 1: decode through the extend kernel: sequence b owns query row b alone
+  // (one row if kv_lens[b] > 0, none otherwise; qo_indptr is not read), and
+  // the rows of empty sequences are written as zeros with lse = -inf
+  int decode_rows;
   ExtendPlanWs ws;
 };
 

@@ -42,7 +42,7 @@ int hip_fail(hipError_t e, const char* what) {
 struct EnvDefaults {
   int split_tokens = 0;
   int prefix_share = RL_PREFIX_AUTO;
-  int validate = 0;
+  int deterministic = 0;
   int target_wgs_per_cu = 64;
   int workers_per_cu = 0;   // 0: as many as are resident at once
   bool fail_alloc = false;
@@ -53,7 +53,7 @@ const EnvDefaults& env() {
     EnvDefaults e;
     if (const char* s = std::getenv("RL_ATTN_SPLIT_TOKENS")) e.split_tokens = std::atoi(s);
     if (const char* s = std::getenv("RL_ATTN_PREFIX_SHARE")) e.prefix_share = std::strcmp(s, "off") == 0;
-    if (const char* s = std::getenv("RL_ATTN_VALIDATE")) e.validate = std::atoi(s) != 0;
+    if (const char* s = std::getenv("RL_ATTN_DETERMINISTIC")) e.deterministic = std::atoi(s) != 0;
     if (const char* s = std::getenv("RL_ATTN_TARGET_WGS_PER_CU")) e.target_wgs_per_cu = std::max(1, std::atoi(s));
     if (const char* s = std::getenv("RL_ATTN_WORKERS_PER_CU")) e.workers_per_cu = std::max(0, std::atoi(s));
     if (const char* s = std::getenv("RL_ATTN_TEST_FAIL_ALLOC")) e.fail_alloc = std::atoi(s) != 0;
@@ -63,24 +63,27 @@ const EnvDefaults& env() {
 }
 
 struct Opts {
-  int split_tokens, prefix_share, validate;
+  int split_tokens, prefix_share, deterministic;
 };
 
 int read_opts(const rl_attn_opts* o, Opts* out) {
   const EnvDefaults& e = env();
-  *out = {e.split_tokens, e.prefix_share, e.validate};
+  *out = {e.split_tokens, e.prefix_share, e.deterministic};
   if (!o) return RL_OK;
-  for (int i = 0; i < 5; ++i)
+  for (int i = 0; i < 4; ++i)
     if (o->reserved[i] != 0) return fail(RL_ERR_INVALID_ARG, "opts.reserved[%d] must be zero", i);
   if (o->split_tokens < 0 || o->split_tokens % 64 != 0)
     return fail(RL_ERR_INVALID_ARG, "opts.split_tokens must be 0 or a positive multiple of 64 (got %d)",
                 o->split_tokens);
   if (o->prefix_share != RL_PREFIX_AUTO && o->prefix_share != RL_PREFIX_OFF)
     return fail(RL_ERR_INVALID_ARG, "opts.prefix_share must be RL_PREFIX_AUTO or RL_PREFIX_OFF");
+  // validate: kept in the struct; page ids are always checked where read
   if (o->validate != 0 && o->validate != 1) return fail(RL_ERR_INVALID_ARG, "opts.validate must be 0 or 1");
+  if (o->deterministic != 0 && o->deterministic != 1)
+    return fail(RL_ERR_INVALID_ARG, "opts.deterministic must be 0 or 1");
   if (o->split_tokens) out->split_tokens = o->split_tokens;
   out->prefix_share = o->prefix_share;
-  out->validate = o->validate || e.validate;
+  out->deterministic = o->deterministic || e.deterministic;
   return RL_OK;
 }
 
@@ -428,6 +431,56 @@ int check_lse(const rl_tensor* lse, int64_t rows, int64_t heads) {
   return RL_OK;
 }
 
+// ------------------------------------------------------------------- extend
+struct ExtendShape {
+  int rows_head, tile_tokens, head_blocks;
+};
+
+// query rows per extend work unit: eight waves of 32 rows
+constexpr int kExtendRows = 256;
+
+ExtendShape extend_shape(int64_t R) {
+  ExtendShape s;
+  s.rows_head = (int)std::min<int64_t>(R, kExtendRows);
+  s.tile_tokens = std::max(1, kExtendRows / s.rows_head);
+  s.head_blocks = (int)((R + s.rows_head - 1) / s.rows_head);
+  return s;
+}
+
+// Work units are (sequence, KV head, head block, chunk tile): at most
+// Hkv * head_blocks * (B + ceil(total_q / tile_tokens)).
+size_t extend_ws_bytes(int64_t B, int64_t total_q, int64_t Hkv, int64_t R, int* max_items) {
+  const ExtendShape s = extend_shape(R);
+  const int64_t items = Hkv * s.head_blocks * (B + (total_q + s.tile_tokens - 1) / s.tile_tokens);
+  *max_items = (int)std::min<int64_t>(items, INT32_MAX / 2);
+  return 256 + align256((size_t)*max_items * 16);
+}
+
+// Work-unit shape, workspace and launch of an extend call whose arguments
+// (pages, q, lengths, output) are already filled in. prof_kind: which timing
+// slot the attention kernel is counted under.
+int run_extend(rl::ExtendArgs& a, hipStream_t st, int prof_kind) {
+  int max_items = 0;
+  const size_t bytes = extend_ws_bytes(a.B, a.total_q, a.Hkv, a.R, &max_items);
+  Workspace* w = nullptr;
+  RL_TRY(acquire_ws(st, bytes, &w));
+  char* base = static_cast<char*>(w->ptr);
+  const ExtendShape s = extend_shape(a.R);
+  a.rows_head = s.rows_head;
+  a.tile_tokens = s.tile_tokens;
+  a.head_blocks = s.head_blocks;
+  a.max_items = max_items;
+  a.ws.hdr = reinterpret_cast<int*>(base);
+  a.ws.items = reinterpret_cast<int4*>(base + 256);
+  a.ws.err = w->err;
+  rl::KernelTimer slot;
+  rl::KernelTimer* timer = prof_timer(&slot);
+  hipError_t e = rl::launch_extend(a, st, timer);
+  prof_commit(prof_kind, timer);
+  if (e != hipSuccess) return hip_fail(e, "extend kernel launch");
+  return RL_OK;
+}
+
 int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages, int kv_dtype,
                 const rl_tensor* k_scale, const rl_tensor* v_scale, const rl_tensor* block_table,
                 const rl_tensor* seq_lens, float scale, rl_tensor* out, rl_tensor* lse_out, const rl_attn_opts* opts,
@@ -457,6 +510,34 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   if (B == 0) return RL_OK;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if (o.deterministic) {
+    // one extend row per sequence: the same kernel and per-row arithmetic as
+    // extend, with no split of the keys, so the result of a sequence does not
+    // depend on the rest of the batch and equals extend's bitwise
+    rl::ExtendArgs e{};
+    e.kv = a.kv;
+    e.q = q->data;
+    e.q_st = q->strides[0];
+    e.q_sh = q->strides[1];
+    e.qo_indptr = nullptr;
+    e.kv_lens = static_cast<const int*>(seq_lens->data);
+    e.kv_lens_s = seq_lens->strides[0];
+    e.B = (int)B;
+    e.total_q = (int)B;
+    e.Hq = (int)Hq;
+    e.Hkv = (int)Hkv;
+    e.R = (int)(Hq / Hkv);
+    e.scale = scale;
+    e.out = out->data;
+    e.out_f32 = is_f32;
+    e.out_st = out->strides[0];
+    e.out_sh = out->strides[1];
+    e.lse = lse_out ? static_cast<float*>(lse_out->data) : nullptr;
+    e.lse_st = lse_out ? lse_out->strides[0] : 0;
+    e.lse_sh = lse_out ? lse_out->strides[1] : 0;
+    e.decode_rows = 1;
+    return run_extend(e, st, 0);
+  }
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -491,7 +572,6 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   a.group_cap = lay.group_cap;
   a.prefix_grid = 2 * cus;
   a.item_waves = decode_item_waves(Hq, Hkv);
-  a.validate = o.validate;
   a.ws.hdr = reinterpret_cast<int*>(base);
   a.ws.nparts = reinterpret_cast<int*>(base + lay.off_nparts);
   a.ws.base = reinterpret_cast<int*>(base + lay.off_base);
@@ -509,31 +589,6 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   prof_commit(0, timer);
   if (e != hipSuccess) return hip_fail(e, "decode kernel launch");
   return RL_OK;
-}
-
-// ------------------------------------------------------------------- extend
-struct ExtendShape {
-  int rows_head, tile_tokens, head_blocks;
-};
-
-// query rows per extend work unit: eight waves of 32 rows
-constexpr int kExtendRows = 256;
-
-ExtendShape extend_shape(int64_t R) {
-  ExtendShape s;
-  s.rows_head = (int)std::min<int64_t>(R, kExtendRows);
-  s.tile_tokens = std::max(1, kExtendRows / s.rows_head);
-  s.head_blocks = (int)((R + s.rows_head - 1) / s.rows_head);
-  return s;
-}
-
-// Work units are (sequence, KV head, head block, chunk tile): at most
-// Hkv * head_blocks * (B + ceil(total_q / tile_tokens)).
-size_t extend_ws_bytes(int64_t B, int64_t total_q, int64_t Hkv, int64_t R, int* max_items) {
-  const ExtendShape s = extend_shape(R);
-  const int64_t items = Hkv * s.head_blocks * (B + (total_q + s.tile_tokens - 1) / s.tile_tokens);
-  *max_items = (int)std::min<int64_t>(items, INT32_MAX / 2);
-  return 256 + align256((size_t)*max_items * 16);
 }
 
 int extend_impl(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor* k_pages, const rl_tensor* v_pages,
@@ -572,12 +627,6 @@ int extend_impl(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor*
   if (B == 0 || total_q == 0) return RL_OK;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
-  int max_items = 0;
-  const size_t bytes = extend_ws_bytes(B, total_q, Hkv, Hq / Hkv, &max_items);
-  Workspace* w = nullptr;
-  RL_TRY(acquire_ws(st, bytes, &w));
-  char* base = static_cast<char*>(w->ptr);
-  const ExtendShape s = extend_shape(Hq / Hkv);
   a.q = q->data;
   a.q_st = q->strides[0];
   a.q_sh = q->strides[1];
@@ -590,9 +639,6 @@ int extend_impl(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor*
   a.Hq = (int)Hq;
   a.Hkv = (int)Hkv;
   a.R = (int)(Hq / Hkv);
-  a.rows_head = s.rows_head;
-  a.tile_tokens = s.tile_tokens;
-  a.head_blocks = s.head_blocks;
   a.scale = scale;
   a.out = out->data;
   a.out_f32 = is_f32;
@@ -601,17 +647,7 @@ int extend_impl(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor*
   a.lse = lse_out ? static_cast<float*>(lse_out->data) : nullptr;
   a.lse_st = lse_out ? lse_out->strides[0] : 0;
   a.lse_sh = lse_out ? lse_out->strides[1] : 0;
-  a.max_items = max_items;
-  a.validate = o.validate;
-  a.ws.hdr = reinterpret_cast<int*>(base);
-  a.ws.items = reinterpret_cast<int4*>(base + 256);
-  a.ws.err = w->err;
-  rl::KernelTimer slot;
-  rl::KernelTimer* timer = prof_timer(&slot);
-  hipError_t e = rl::launch_extend(a, st, timer);
-  prof_commit(1, timer);
-  if (e != hipSuccess) return hip_fail(e, "extend kernel launch");
-  return RL_OK;
+  return run_extend(a, st, 1);
 }
 
 }  // namespace
@@ -751,8 +787,11 @@ size_t rl_attn_decode_workspace_size(int64_t batch, int64_t num_q_heads, int64_t
   if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0) return 0;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess) cus = device_cus(dev);
-  // bf16 and FP8 pages may keep different numbers of workers resident: the larger layout
-  size_t total = 0;
+  // bf16 and FP8 pages may keep different numbers of workers resident, and a
+  // deterministic decode uses the extend work list: the largest of the three
+  int mi = 0;
+  const int64_t R = num_q_heads / num_kv_heads;
+  size_t total = R >= 1 ? extend_ws_bytes(batch, batch, num_kv_heads, R, &mi) : 0;
   for (bool fp8 : {false, true})
     total = std::max(total, decode_layout(batch, num_q_heads, num_kv_heads, max_pages, page_size, env().split_tokens,
                                           cus, env().prefix_share == RL_PREFIX_AUTO, fp8)

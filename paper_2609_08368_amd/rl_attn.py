@@ -37,7 +37,7 @@ class RlTensor(ctypes.Structure):
 
 class RlOpts(ctypes.Structure):
     _fields_ = [("split_tokens", ctypes.c_int32), ("prefix_share", ctypes.c_int32),
-                ("validate", ctypes.c_int32), ("reserved", ctypes.c_int32 * 5)]
+                ("validate", ctypes.c_int32), ("deterministic", ctypes.c_int32), ("reserved", ctypes.c_int32 * 4)]
 
 
 class RlAttnError(RuntimeError):
@@ -138,20 +138,21 @@ def _stream(stream) -> Optional[int]:
     return getattr(stream, "cuda_stream", stream)
 
 
-def _opts(split_tokens=0, prefix_share=True, validate=False):
+def _opts(split_tokens=0, prefix_share=True, validate=False, deterministic=False):
     o = RlOpts()
     o.split_tokens = int(split_tokens)
     o.prefix_share = RL_PREFIX_AUTO if prefix_share else RL_PREFIX_OFF
     o.validate = int(bool(validate))
+    o.deterministic = int(bool(deterministic))
     return o
 
 
 def decode(q, k_pages, v_pages, block_table, seq_lens, scale, out=None, lse=None, *, split_tokens=0,
-           prefix_share=True, validate=False, stream=None):
+           prefix_share=True, validate=False, deterministic=False, stream=None):
     """``rl_attn_decode_ex``: returns ``out`` (and fills ``lse`` if given)."""
     if out is None:
         out = torch.empty_like(q)
-    o = _opts(split_tokens, prefix_share, validate)
+    o = _opts(split_tokens, prefix_share, validate, deterministic)
     _check(lib().rl_attn_decode_ex(_ref(view(q)), _ref(view(k_pages)), _ref(view(v_pages)),
                                    _ref(view(block_table)), _ref(view(seq_lens)), ctypes.c_float(scale),
                                    _ref(view(out)), _ref(view(lse)), ctypes.byref(o), _stream(stream)))
@@ -192,11 +193,11 @@ def extend_plain(q, qo_indptr, k_pages, v_pages, block_table, kv_lens, scale, ou
 
 
 def decode_fp8(q, k_pages, v_pages, k_scale, v_scale, block_table, seq_lens, scale, out=None, lse=None, *,
-               split_tokens=0, prefix_share=True, validate=False, stream=None):
+               split_tokens=0, prefix_share=True, validate=False, deterministic=False, stream=None):
     """``rl_attn_decode_fp8``: pages are ``torch.float8_e4m3fn``, scales ``[Hkv]`` float32."""
     if out is None:
         out = torch.empty_like(q)
-    o = _opts(split_tokens, prefix_share, validate)
+    o = _opts(split_tokens, prefix_share, validate, deterministic)
     _check(lib().rl_attn_decode_fp8(_ref(view(q)), _ref(view(k_pages)), _ref(view(v_pages)), _ref(view(k_scale)),
                                     _ref(view(v_scale)), _ref(view(block_table)), _ref(view(seq_lens)),
                                     ctypes.c_float(scale), _ref(view(out)), _ref(view(lse)), ctypes.byref(o),

@@ -88,7 +88,7 @@ def test_decode_validation(mutate, code, needle):
 
 @pytest.mark.parametrize("field,value,needle", [
     ("split_tokens", 100, "split_tokens"), ("split_tokens", -64, "split_tokens"),
-    ("prefix_share", 7, "prefix_share"), ("validate", 2, "validate")])
+    ("prefix_share", 7, "prefix_share"), ("validate", 2, "validate"), ("deterministic", -1, "deterministic")])
 def test_option_validation(field, value, needle):
     a = decode_args()
     o = ra.RlOpts()
