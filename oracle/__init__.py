@@ -15,7 +15,9 @@ What it computes (the plain definition, evaluated directly in float64):
   causally, to the chunk itself ("each turn prefills only the newly generated
   suffix", same section, and the session server of section "Token-In-Token-Out");
 * merge   -- the log-sum-exp combination of attention results over disjoint
-  key ranges (split-KV partials).
+  key ranges (split-KV partials);
+* append  -- writing new tokens' K/V rows into their pages (``kv_append``),
+  with the FP8 E4M3 encoding of the quotient by the KV head's scale.
 
 Pages hold bf16 values, or OCP FP8 E4M3 codes with one dequantisation scale
 per KV head (the FP8 key-value cache of the paper's case-study rollout,
@@ -31,7 +33,9 @@ single-key exactness, uniform-key closed form, page-size/page-order
 invariance, split/merge identity, extend<->decode and causal brute force,
 GQA expansion, scale homogeneity, batch permutation, closed-form golden file,
 FP8 E4M3 decoding against torch's float8_e4m3fn and the format's closed forms,
-FP8 pages against the same values in bf16, per-KV-head scales).
+FP8 pages against the same values in bf16, per-KV-head scales; KV append
+positions against a removal/append round trip, and the E4M3 encoder against
+torch's float8_e4m3fn cast, its own decoder and brute-force nearest values).
 Parity with values printed in the paper is unpinned: the paper prints none.
 """
 
@@ -45,3 +49,4 @@ from .attention import (  # noqa: F401
     fp8_e4m3_to_f64,
     merge,
 )
+from .kv_append import append_kv, fp8_e4m3_encode, quantize_rows  # noqa: F401

@@ -18,7 +18,12 @@ a deliberately broken copy of it in the mutation tests) and raises
 * FP8 E4M3 KV pages: every code against torch's independent float8_e4m3fn
   conversion and the format's closed forms; with unit scales the result equals
   the bf16 oracle on the same values bitwise; per-KV-head power-of-two scales
-  equal exactly scaled bf16 pages; arbitrary scales agree with brute force.
+  equal exactly scaled bf16 pages; arbitrary scales agree with brute force;
+* KV append: clearing and re-appending the last rows restores the pages
+  bitwise; the E4M3 encoder against torch's float8_e4m3fn cast (values,
+  midpoints, both signs), round trips, brute-force nearest values and
+  saturation; FP8 append writes torch's cast of the float32 quotient, only at
+  the new positions.
 
 The paper prints no attention values, so parity with printed values is
 unpinned; the closed-form golden file in ``tests/golden`` stands in for a
@@ -426,6 +431,104 @@ def pin_fp8_scales(orc, seed=10):
             assert abs(l8[b, h] - scipy.special.logsumexp(s)) < 1e-12 * max(1.0, abs(l8[b, h]))
 
 
+def _fp8_encode_torch(x: np.ndarray) -> np.ndarray:
+    """torch's float8_e4m3fn cast (round to nearest even) as uint8 codes; an independent encoder."""
+    import torch
+
+    return torch.from_numpy(np.asarray(x, np.float32).copy()).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+
+
+def pin_fp8_encode(orc, seed=11):
+    rng = np.random.default_rng(seed)
+    # every finite value and every midpoint between neighbours (exact in float32), both signs
+    finite = _fp8_values_torch(np.arange(0x7F, dtype=np.uint8))
+    mids = (finite[:-1] + finite[1:]) / 2
+    mag = np.exp2(rng.uniform(-12, np.log2(448.0), 4000))
+    x = np.concatenate([finite, mids, mag, [0.0, 440.0, 447.9, 448.0]]).astype(np.float32)
+    x = np.concatenate([x, -x])
+    got = orc.fp8_e4m3_encode(x)
+    assert np.array_equal(got, _fp8_encode_torch(x)), "E4M3 encoding differs from torch's float8_e4m3fn cast"
+    # round trip of every finite code, and brute-force nearest with ties to the even code
+    codes = np.array([c for c in range(256) if c & 0x7F != 0x7F], dtype=np.uint8)
+    assert np.array_equal(orc.fp8_e4m3_encode(_fp8_values_torch(codes).astype(np.float32)), codes)
+    y = (rng.standard_normal(2000) * np.exp2(rng.uniform(-10, 8, 2000))).astype(np.float32)
+    y = y[np.abs(y) <= 448]
+    dec = _fp8_values_torch(orc.fp8_e4m3_encode(y))
+    dist = np.abs(y.astype(np.float64)[:, None] - np.concatenate([finite, -finite])[None, :])
+    assert np.all(np.abs(dec - y) <= dist.min(axis=1)), "not the nearest E4M3 value"
+    # saturation and NaN
+    sat = orc.fp8_e4m3_encode(np.array([449.0, 480.0, 1e6, np.inf, -500.0, -np.inf], np.float32))
+    assert list(sat) == [0x7E] * 4 + [0xFE] * 2, "magnitudes above 448 must saturate"
+    assert orc.fp8_e4m3_encode(np.array([np.nan], np.float32))[0] & 0x7F == 0x7F
+
+
+def _append_problem(rng, lens=(40, 9, 71, 16), chunk=(7, 9, 1, 16), hkv=2, page_size=8):
+    lens = np.array(lens, np.int32)
+    rows = to_bf16_bits(rng.standard_normal((len(lens), int(lens.max()), hkv, D)))
+    vrows = to_bf16_bits(rng.standard_normal((len(lens), int(lens.max()), hkv, D)))
+    kp, bt = pack_pages(rows, lens, page_size, np.random.default_rng(99))
+    vp, _ = pack_pages(vrows, lens, page_size, np.random.default_rng(99))
+    n = np.array(chunk, np.int32)
+    qo = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
+    k_new = np.concatenate([rows[b, lens[b] - n[b]:lens[b]] for b in range(len(lens))])
+    v_new = np.concatenate([vrows[b, lens[b] - n[b]:lens[b]] for b in range(len(lens))])
+    return rows, vrows, kp, vp, bt, lens, qo, k_new, v_new
+
+
+def pin_append_roundtrip(orc, seed=12):
+    """Clearing the last n_b rows of each sequence and appending them again restores the pages bitwise."""
+    rng = np.random.default_rng(seed)
+    _, _, kp, vp, bt, lens, qo, k_new, v_new = _append_problem(rng)
+    kc, vc = kp.copy(), vp.copy()
+    for b in range(len(lens)):
+        n = int(qo[b + 1] - qo[b])
+        for t in range(int(lens[b]) - n, int(lens[b])):
+            kc[bt[b, t // 8], t % 8] = 0x1234
+            vc[bt[b, t // 8], t % 8] = 0x4321
+    ka, va = orc.append_kv(kc, vc, bt, lens, qo, k_new, v_new)
+    assert np.array_equal(ka, kp) and np.array_equal(va, vp), "append does not restore the removed rows"
+    assert not np.array_equal(kc, kp), "the problem must clear something"
+
+
+def pin_append_fp8(orc, seed=13):
+    """FP8 pages receive torch's E4M3 cast of the float32 quotient by the head's scale, and only
+    at the appended positions; dequantised values are within half an E4M3 step of the input."""
+    rng = np.random.default_rng(seed)
+    rows, vrows, _, _, bt, lens, qo, k_new, v_new = _append_problem(rng)
+    pool = np.full((bt.max() + 3, 8, 2, D), 0x5A, np.uint8)
+    # |x| / scale stays below 448 (torch's cast does not saturate; saturation is pinned above)
+    ks = np.array([0.013, 0.021], np.float32)
+    vs = np.array([0.017, 0.0125], np.float32)
+    ka, va = orc.append_kv(pool, pool, bt, lens, qo, k_new, v_new, k_scale=ks, v_scale=vs)
+    for pages, new, sc in ((ka, k_new, ks), (va, v_new, vs)):
+        quot = (from_bits(new).astype(np.float32) / sc[None, :, None]).astype(np.float32)
+        assert np.abs(quot).max() < 448
+        want = _fp8_encode_torch(quot)
+        touched = np.zeros(pool.shape[:2], bool)
+        r = 0
+        for b in range(len(lens)):
+            n = int(qo[b + 1] - qo[b])
+            for i in range(n):
+                t = int(lens[b]) - n + i
+                p, s = bt[b, t // 8], t % 8
+                assert np.array_equal(pages[p, s], want[r]), "appended codes"
+                touched[p, s] = True
+                r += 1
+        assert np.all(pages[~touched] == 0x5A), "append wrote outside the new positions"
+        x = from_bits(new)
+        deq = _fp8_values_torch(want) * sc[None, :, None].astype(np.float64)
+        assert np.all(np.abs(deq - x) <= np.abs(x) / 16 + 2.0 ** -10 * sc.max()), "dequantisation error"
+    # near-ties found by search, where the rounding of the quotient decides the code: the
+    # float32 quotient x / s, not x times the reciprocal of s, and not the exact quotient
+    tie = np.zeros((1, 2, D), np.uint16)
+    tie[0, 0, :2] = [0x3B90, 0x3B60]
+    tie[0, 1, :3] = [0x3A80, 0x3BA0, 0x3C10]
+    sc = np.array([0.3, 1 / 3], np.float32)
+    quot = (from_bits(tie).astype(np.float32) / sc[None, :, None]).astype(np.float32)
+    assert np.array_equal(orc.quantize_rows(tie, sc), _fp8_encode_torch(quot)), "quotient rounding"
+
+
 ALL_PINS = [pin_brute_force, pin_single_key, pin_uniform_keys, pin_page_invariance, pin_split_merge,
             pin_extend, pin_gqa_expansion, pin_scale_homogeneity, pin_batch_and_sharing, pin_golden,
-            pin_fp8_codes, pin_fp8_equals_bf16, pin_fp8_scales]
+            pin_fp8_codes, pin_fp8_equals_bf16, pin_fp8_scales, pin_fp8_encode, pin_append_roundtrip,
+            pin_append_fp8]
