@@ -324,6 +324,63 @@ def deterministic_study(steps: int, warmup: int, w, t, split_ms: float) -> dict:
     return res
 
 
+def append_study(steps: int, warmup: int, w_ext, w_dec) -> dict:
+    """Time KV append: the multi-turn batch's chunk tokens, and one decode step's tokens of
+    the ragged batch, into bf16 and FP8 pages (new rows resident in HBM)."""
+    import torch
+
+    from paper_2609_08368_amd import rl_attn as ra
+    from paper_2609_08368_amd import workloads as wl
+
+    dev = torch.device("cuda:0")
+    res = {}
+    for wname, w in (("extend_chunks", w_ext), ("decode_step", w_dec)):
+        total = w.total_q if w.kind == "extend" else w.batch
+        g = torch.Generator(device=dev)
+        g.manual_seed(77)
+        k = torch.randn((total, w.hkv, 128), generator=g, device=dev).to(torch.bfloat16)
+        v = torch.randn((total, w.hkv, 128), generator=g, device=dev).to(torch.bfloat16)
+        for fp8 in (False, True):
+            t = (wl.materialize_fp8 if fp8 else wl.materialize)(w, dev, poison=False)
+            if w.kind == "extend":
+                indptr = t["qo_indptr"]
+            else:
+                indptr = torch.arange(w.batch + 1, dtype=torch.int32, device=dev)
+
+            def fn():
+                if fp8:
+                    ra.append_kv_fp8(k, v, indptr, t["block_table"], t["kv_lens"], t["k_pages"], t["v_pages"],
+                                     t["k_scale"], t["v_scale"])
+                else:
+                    ra.append_kv(k, v, indptr, t["block_table"], t["kv_lens"], t["k_pages"], t["v_pages"])
+
+            for _ in range(warmup):
+                fn()
+            torch.cuda.synchronize()
+            stream = torch.cuda.current_stream()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            ra.profile_read("append")
+            ra.profile_enable(True)
+            a.record(stream)
+            for _ in range(steps):
+                fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            ra.profile_enable(False)
+            _, kern_ms = ra.profile_read("append")
+            ms = a.elapsed_time(b) / steps
+            elems = 2 * total * w.hkv * 128
+            moved = elems * 2 + elems * (1 if fp8 else 2)        # read bf16 rows, write pages
+            res[f"{wname}_{'fp8' if fp8 else 'bf16'}"] = {
+                "rows": total, "ms_per_call": round(ms, 5), "kernel_ms": round(kern_ms, 5), "bytes": moved,
+                "kernel_GBps": round(moved / (kern_ms * 1e-3) / 1e9, 1),
+                "hbm_frac": round(moved / (kern_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)}
+            del t
+            torch.cuda.empty_cache()
+    log(f"append: {res}")
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -494,6 +551,7 @@ def main():
     torch.cuda.empty_cache()
     result["deterministic_decode"] = deterministic_study(args.steps, args.warmup, w_dec, t_dec,
                                                          mean["decode_ragged"])
+    result["kv_append"] = append_study(args.steps, args.warmup, w_ext, w_dec)
     result["fp8_kv"] = fp8_study(args.steps, args.warmup, w_dec, w_ext, mean["decode_ragged"],
                                  mean["extend_multiturn"])
     # measured ceilings on this device, beside the specification peaks

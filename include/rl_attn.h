@@ -175,6 +175,34 @@ int rl_attn_extend_fp8(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_
                        const rl_tensor* block_table, const rl_tensor* kv_lens, float scale, rl_tensor* out,
                        rl_tensor* lse_out, const rl_attn_opts* opts, void* stream);
 
+/* KV append (paper: each agentic turn prefills only its newly appended
+ * suffix, section "Fast Agentic Rollout with SGLang", and every decode step
+ * adds one token): writes the new tokens' K and V rows into their pages, in
+ * the addressing the attention calls use.
+ *   k_new, v_new [total_new, Hkv, 128] bf16: rows qo_indptr[b] .. qo_indptr[b+1]-1
+ *                are sequence b's new tokens, in order
+ *   qo_indptr    [B+1] int32, non-decreasing from 0 to total_new
+ *   block_table  [B, max_pages] int32 (the pages of the new positions must be assigned)
+ *   kv_lens      [B] int32: tokens of sequence b after the append (>= n_b); new
+ *                row i of sequence b goes to logical position kv_lens[b] - n_b + i
+ *   k_pages, v_pages [num_pages, P, Hkv, 128]: only the new positions are written
+ * The bf16 call copies the rows. The FP8 call takes E4M3 pages and the
+ * per-KV-head scales of rl_attn_decode_fp8 and writes, for each element x of
+ * KV head g, the E4M3 code nearest to the float32 quotient x / scale[g] (ties
+ * to the even code; magnitudes above 448 saturate to 448). A row whose page id,
+ * length or indptr is out of range (or whose scale is not positive and finite)
+ * is not written and is reported by rl_attn_check_device_errors(); rows that
+ * map to the same position race. Asynchronous on `stream`; allocates nothing
+ * beyond the library's per-stream error word. */
+int rl_attn_append_kv(const rl_tensor* k_new, const rl_tensor* v_new, const rl_tensor* qo_indptr,
+                      const rl_tensor* block_table, const rl_tensor* kv_lens, rl_tensor* k_pages,
+                      rl_tensor* v_pages, void* stream);
+
+int rl_attn_append_kv_fp8(const rl_tensor* k_new, const rl_tensor* v_new, const rl_tensor* qo_indptr,
+                          const rl_tensor* block_table, const rl_tensor* kv_lens, rl_tensor* k_pages,
+                          rl_tensor* v_pages, const rl_tensor* k_scale, const rl_tensor* v_scale,
+                          void* stream);
+
 /* Log-sum-exp merge of partial attention results over disjoint key ranges
  * (the split-KV combine, exposed for testing and for callers that split work
  * themselves):
@@ -207,12 +235,13 @@ size_t rl_attn_extend_workspace_size(int64_t batch, int64_t total_q, int64_t num
                                      int64_t num_kv_heads, int64_t max_pages, int64_t page_size);
 
 /* Kernel timing for benchmarks and profiling tools. While enabled, each
- * decode / extend call brackets its main attention kernel with a pair of HIP
+ * decode / extend / append call brackets its main kernel with a pair of HIP
  * events on the call's stream (the planner and combine kernels are outside
  * the pair). rl_attn_profile_read() waits for the recorded events and returns
  * the number of timed launches and their mean duration in milliseconds per
- * kind (kind 0 = decode attention kernel, 1 = extend attention kernel), then
- * forgets them. Disabled by default; enabling costs two event records per call. */
+ * kind (kind 0 = decode attention kernel, 1 = extend attention kernel, 2 =
+ * KV append kernel; a deterministic decode counts as kind 0), then forgets
+ * them. Disabled by default; enabling costs two event records per call. */
 int rl_attn_profile_enable(int on);
 int rl_attn_profile_read(int kind, int* launches, double* mean_ms);
 

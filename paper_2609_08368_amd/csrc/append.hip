@@ -1,0 +1,171 @@
+// KV append: the new tokens' K and V rows (an appended turn's suffix, or one
+// decode step's token) are written into their pages before attention reads
+// them. Sequence b owns new rows qo_indptr[b] .. qo_indptr[b+1]-1 and holds
+// kv_lens[b] tokens after the append, so new row i goes to logical position
+// kv_lens[b] - n_b + i. FP8 pages receive the E4M3 code of the row divided
+// by the KV head's scale.
+//
+// A thread moves one 8-element column of up to 8 KV heads of one new row: the
+// 16 threads of a head row read and write 256 contiguous bytes (128 for FP8),
+// and each thread has 16 row loads in flight before it looks up the page. The
+// work is a copy: HBM-bound at 4 (bf16) or 3 (FP8) bytes moved per element.
+#include "attn_common.hpp"
+#include "kernels.hpp"
+
+namespace rl {
+
+namespace {
+
+constexpr int kAppendThreads = 256;
+constexpr int kGroup = 8;               // KV heads per thread (same column of each head row)
+
+// OCP E4M3 code of a float32 value, from the format's bit layout: nearest
+// value, ties to the even code; magnitudes of 448 and above (infinity
+// included) saturate to 448; NaN gives the NaN code. The sign is kept.
+__device__ __forceinline__ uint32_t e4m3_from_f32(float f) {
+  const uint32_t u = __float_as_uint(f);
+  const uint32_t sign = (u >> 24) & 0x80u;
+  const uint32_t a = u & 0x7FFFFFFFu;
+  uint32_t code;
+  if (a > 0x7F800000u) {
+    code = 0x7Fu;                                   // NaN
+  } else if (a >= 0x43E00000u) {
+    code = 0x7Eu;                                   // >= 448: saturate
+  } else if (a < 0x3C800000u) {
+    // below 2^-6: the subnormal step is 2^-9, so the code is the value in
+    // steps, rounded to nearest even (8 is the smallest normal, code 0x08)
+    code = (uint32_t)__builtin_rintf(__uint_as_float(a) * 512.f);
+  } else {
+    const uint32_t e = (a >> 23) - 127u + 7u;       // biased E4M3 exponent, 1..15
+    uint32_t r = (a >> 20) & 7u;                    // top three mantissa bits
+    const uint32_t rest = a & 0xFFFFFu;
+    if (rest > 0x80000u || (rest == 0x80000u && (r & 1u))) ++r;
+    code = (e << 3) + r;                            // r == 8 carries into the exponent
+    if (code > 0x7Eu) code = 0x7Eu;
+  }
+  return code | sign;
+}
+
+// E4M3 codes of eight bf16 values divided by the positive scale s (inv: the
+// correctly rounded 1/s), four per word. The code is the E4M3 value nearest
+// to the correctly rounded float32 quotient. Fast path: q0 = x * inv, then
+// one residual correction q0 + (x - q0 s) inv, which is the correctly rounded
+// quotient for normal results (Markstein's theorem: the residual is exact in
+// an FMA and the reciprocal is correctly rounded); subnormal quotients, where
+// it may be off, all encode to zero, and the sign is taken from x so that -0
+// stays -0. The clamped value is then converted by the hardware E4M3
+// conversion (round to nearest even), which matches the format's definition
+// on every input in that range. Non-finite inputs, or a product that
+// overflows, take the IEEE division and the bit-level encoder instead.
+__device__ __forceinline__ uint2 e4m3_pack8(const bf16x8& x, float s, float inv) {
+  float q[8];
+  bool special = false;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float xf = (float)x[e];
+    const float q0 = xf * inv;
+    const float r = __builtin_fmaf(-q0, s, xf);
+    q[e] = __builtin_copysignf(__builtin_fmaf(r, inv, q0), xf);
+    special |= (__float_as_uint(q0) & 0x7F800000u) == 0x7F800000u;
+  }
+  uint2 w;
+  if (!special) {
+    auto c = [&](int e) { return __builtin_amdgcn_fmed3f(q[e], -448.f, 448.f); };
+    w.x = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c(0), c(1), 0, false);
+    w.x = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c(2), c(3), (int)w.x, true);
+    w.y = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c(4), c(5), 0, false);
+    w.y = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c(6), c(7), (int)w.y, true);
+  } else {
+    w.x = w.y = 0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t code = e4m3_from_f32((float)x[e] / s);
+      if (e < 4) w.x |= code << (8 * e); else w.y |= code << (8 * (e - 4));
+    }
+  }
+  return w;
+}
+
+template <bool kFp8>
+__global__ __launch_bounds__(kAppendThreads) void append_kernel(AppendArgs a) {
+  // thread -> (new row r, group of up to kGroup KV heads, 8-element column c)
+  const int groups = (a.Hkv + kGroup - 1) / kGroup;
+  const int per_row = groups * (kHeadDim / 8);
+  const int64_t i = (int64_t)blockIdx.x * kAppendThreads + threadIdx.x;
+  if (i >= (int64_t)a.total_new * per_row) return;
+  const int r = (int)(i / per_row);
+  const int rem = (int)(i - (int64_t)r * per_row);
+  const int g0 = (rem / (kHeadDim / 8)) * kGroup, c = rem % (kHeadDim / 8);
+  const int gn = min(kGroup, a.Hkv - g0);
+  // the new rows are read first (always in bounds), so their latency overlaps
+  // the lookups below
+  bf16x8 kx[kGroup], vx[kGroup];
+#pragma unroll
+  for (int j = 0; j < kGroup; ++j) {
+    const int g = g0 + (j < gn ? j : 0);
+    kx[j] = *reinterpret_cast<const bf16x8*>((const __bf16*)a.k_new + r * a.kn_st + g * a.kn_sh + 8 * c);
+    vx[j] = *reinterpret_cast<const bf16x8*>((const __bf16*)a.v_new + r * a.vn_st + g * a.vn_sh + 8 * c);
+  }
+  // owning sequence: the last b with qo_indptr[b] <= r
+  int lo = 0, hi = a.B - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.qo_indptr[(int64_t)mid * a.indptr_s] <= r) lo = mid; else hi = mid - 1;
+  }
+  const int b = lo;
+  const int q0 = a.qo_indptr[(int64_t)b * a.indptr_s];
+  const int q1 = a.qo_indptr[(int64_t)(b + 1) * a.indptr_s];
+  if (r < q0 || r >= q1) {              // qo_indptr not a partition of the new rows
+    atomicOr(a.err, kErrIndptr);
+    return;
+  }
+  const int n = q1 - q0;
+  const int kv = a.kv_lens[(int64_t)b * a.kv_lens_s];
+  if (kv < n || kv > a.max_pages * a.page_size) {
+    atomicOr(a.err, kv < n ? kErrKvShort : kErrLen);
+    return;
+  }
+  const int t = kv - n + (r - q0);
+  const int page = a.bt[(int64_t)b * a.bt_sb + (int64_t)(t >> a.log2_page) * a.bt_sj];
+  if ((unsigned)page >= (unsigned)a.num_pages) {   // never write outside the pool
+    atomicOr(a.err, kErrPage);
+    return;
+  }
+  const int slot = t & (a.page_size - 1);
+  const int64_t kbase = (int64_t)page * a.sp + (int64_t)slot * a.ss + 8 * c;
+  const int64_t vbase = (int64_t)page * a.v_sp + (int64_t)slot * a.v_ss + 8 * c;
+#pragma unroll
+  for (int j = 0; j < kGroup; ++j) {
+    if (j >= gn) break;
+    const int g = g0 + j;
+    const int64_t ko = kbase + (int64_t)g * a.sh, vo = vbase + (int64_t)g * a.v_sh;
+    if constexpr (!kFp8) {
+      *reinterpret_cast<bf16x8*>((__bf16*)a.k + ko) = kx[j];
+      *reinterpret_cast<bf16x8*>((__bf16*)a.v + vo) = vx[j];
+    } else {
+      const float ks = a.k_scale[g * a.ks_s], vs = a.v_scale[g * a.vs_s];
+      if (!(ks > 0.f && ks < __builtin_huge_valf()) || !(vs > 0.f && vs < __builtin_huge_valf())) {
+        atomicOr(a.err, kErrScale);
+        continue;
+      }
+      *reinterpret_cast<uint2*>((uint8_t*)a.k + ko) = e4m3_pack8(kx[j], ks, 1.0f / ks);
+      *reinterpret_cast<uint2*>((uint8_t*)a.v + vo) = e4m3_pack8(vx[j], vs, 1.0f / vs);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_append(const AppendArgs& a, hipStream_t stream, KernelTimer* timer) {
+  const int64_t threads = (int64_t)a.total_new * ((a.Hkv + kGroup - 1) / kGroup) * (kHeadDim / 8);
+  const unsigned grid = (unsigned)((threads + kAppendThreads - 1) / kAppendThreads);
+  if (timer) (void)hipEventRecord(timer->start, stream);
+  if (a.k_scale)
+    append_kernel<true><<<grid, kAppendThreads, 0, stream>>>(a);
+  else
+    append_kernel<false><<<grid, kAppendThreads, 0, stream>>>(a);
+  if (timer) (void)hipEventRecord(timer->stop, stream);
+  return hipGetLastError();
+}
+
+}  // namespace rl

@@ -124,6 +124,27 @@ struct MergeArgs {
   int64_t lo_sn, lo_sh;
 };
 
+// KV append: new rows [total_new, Hkv, 128] bf16 into their pages.
+struct AppendArgs {
+  const void* k_new;
+  const void* v_new;
+  int64_t kn_st, kn_sh, vn_st, vn_sh;
+  void* k;                // pages, written
+  void* v;
+  int64_t sp, ss, sh, v_sp, v_ss, v_sh;
+  const float* k_scale;   // FP8 pages: [Hkv] scales (null for bf16)
+  const float* v_scale;
+  int64_t ks_s, vs_s;
+  const int* bt;
+  int64_t bt_sb, bt_sj;
+  const int* qo_indptr;
+  int64_t indptr_s;
+  const int* kv_lens;
+  int64_t kv_lens_s;
+  int B, total_new, Hkv, num_pages, page_size, log2_page, max_pages;
+  int* err;
+};
+
 // Optional events around the main attention kernel (benchmark timing).
 struct KernelTimer {
   hipEvent_t start = nullptr, stop = nullptr;
@@ -141,5 +162,6 @@ double diag_mfma_flops(int iters, int cus);
 int decode_workers_per_cu(int R, int Hkv, int item_waves, bool fp8);
 hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream, KernelTimer* timer);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t stream);
+hipError_t launch_append(const AppendArgs& a, hipStream_t stream, KernelTimer* timer);
 
 }  // namespace rl

@@ -223,7 +223,7 @@ int acquire_ws(hipStream_t st, size_t need, Workspace** out) {
 struct Profiler {
   std::mutex mu;
   bool on = false;
-  std::vector<rl::KernelTimer> pending[2];
+  std::vector<rl::KernelTimer> pending[3];   // decode, extend, append
 };
 
 Profiler& prof() {
@@ -650,6 +650,84 @@ int extend_impl(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor*
   return run_extend(a, st, 1);
 }
 
+// ------------------------------------------------------------------- append
+int append_impl(const rl_tensor* k_new, const rl_tensor* v_new, const rl_tensor* qo_indptr,
+                const rl_tensor* block_table, const rl_tensor* kv_lens, rl_tensor* k_pages, rl_tensor* v_pages,
+                int kv_dtype, const rl_tensor* k_scale, const rl_tensor* v_scale, void* stream) {
+  RL_TRY(check_view(k_new, "k_new", 3));
+  RL_TRY(check_view(v_new, "v_new", 3));
+  RL_TRY(check_dtype(k_new, "k_new", RL_BF16));
+  RL_TRY(check_dtype(v_new, "v_new", RL_BF16));
+  for (int i = 0; i < 3; ++i)
+    if (k_new->shape[i] != v_new->shape[i]) return fail(RL_ERR_SHAPE, "k_new and v_new shapes differ (dim %d)", i);
+  RL_TRY(check_rows128(k_new, "k_new"));
+  RL_TRY(check_rows128(v_new, "v_new"));
+  RL_TRY(check_view(kv_lens, "kv_lens", 1));
+  RL_TRY(check_dtype(kv_lens, "kv_lens", RL_I32));
+  RL_TRY(check_view(qo_indptr, "qo_indptr", 1));
+  RL_TRY(check_dtype(qo_indptr, "qo_indptr", RL_I32));
+  const int64_t B = kv_lens->shape[0];
+  if (qo_indptr->shape[0] != B + 1)
+    return fail(RL_ERR_SHAPE, "qo_indptr must have batch + 1 = %lld entries (got %lld)", (long long)(B + 1),
+                (long long)qo_indptr->shape[0]);
+  rl::PagedKV kv{};
+  RL_TRY(fill_paged(k_pages, v_pages, block_table, B, kv_dtype, k_scale, v_scale, &kv));
+  const int64_t Hkv = k_pages->shape[2];
+  if (k_new->shape[1] != Hkv)
+    return fail(RL_ERR_SHAPE, "k_new has %lld KV heads, the pages %lld", (long long)k_new->shape[1], (long long)Hkv);
+  const int64_t total_new = k_new->shape[0];
+  if (B > (1 << 22) || total_new > INT32_MAX / 2 || Hkv > 4096)
+    return fail(RL_ERR_UNSUPPORTED, "batch, new rows or head count too large");
+  RL_TRY(check_data(k_new, "k_new"));
+  RL_TRY(check_data(v_new, "v_new"));
+  RL_TRY(check_data(kv_lens, "kv_lens"));
+  RL_TRY(check_data(qo_indptr, "qo_indptr"));
+  if (B == 0 || total_new == 0) return RL_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Workspace* w = nullptr;
+  RL_TRY(acquire_ws(st, 0, &w));          // the error word only
+  rl::AppendArgs a{};
+  a.k_new = k_new->data;
+  a.v_new = v_new->data;
+  a.kn_st = k_new->strides[0];
+  a.kn_sh = k_new->strides[1];
+  a.vn_st = v_new->strides[0];
+  a.vn_sh = v_new->strides[1];
+  a.k = k_pages->data;
+  a.v = v_pages->data;
+  a.sp = kv.sp;
+  a.ss = kv.ss;
+  a.sh = kv.sh;
+  a.v_sp = kv.v_sp;
+  a.v_ss = kv.v_ss;
+  a.v_sh = kv.v_sh;
+  a.k_scale = kv.k_scale;
+  a.v_scale = kv.v_scale;
+  a.ks_s = kv.ks_s;
+  a.vs_s = kv.vs_s;
+  a.bt = kv.bt;
+  a.bt_sb = kv.bt_sb;
+  a.bt_sj = kv.bt_sj;
+  a.qo_indptr = static_cast<const int*>(qo_indptr->data);
+  a.indptr_s = qo_indptr->strides[0];
+  a.kv_lens = static_cast<const int*>(kv_lens->data);
+  a.kv_lens_s = kv_lens->strides[0];
+  a.B = (int)B;
+  a.total_new = (int)total_new;
+  a.Hkv = (int)Hkv;
+  a.num_pages = kv.num_pages;
+  a.page_size = kv.page_size;
+  a.log2_page = kv.log2_page;
+  a.max_pages = kv.max_pages;
+  a.err = w->err;
+  rl::KernelTimer slot;
+  rl::KernelTimer* timer = prof_timer(&slot);
+  hipError_t e = rl::launch_append(a, st, timer);
+  prof_commit(2, timer);
+  if (e != hipSuccess) return hip_fail(e, "append kernel launch");
+  return RL_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -696,6 +774,20 @@ int rl_attn_extend_fp8(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_
                        rl_tensor* lse_out, const rl_attn_opts* opts, void* stream) {
   return extend_impl(q, qo_indptr, k_pages, v_pages, RL_FP8_E4M3, k_scale, v_scale, block_table, kv_lens, scale, out,
                      lse_out, opts, stream);
+}
+
+int rl_attn_append_kv(const rl_tensor* k_new, const rl_tensor* v_new, const rl_tensor* qo_indptr,
+                      const rl_tensor* block_table, const rl_tensor* kv_lens, rl_tensor* k_pages, rl_tensor* v_pages,
+                      void* stream) {
+  return append_impl(k_new, v_new, qo_indptr, block_table, kv_lens, k_pages, v_pages, RL_BF16, nullptr, nullptr,
+                     stream);
+}
+
+int rl_attn_append_kv_fp8(const rl_tensor* k_new, const rl_tensor* v_new, const rl_tensor* qo_indptr,
+                          const rl_tensor* block_table, const rl_tensor* kv_lens, rl_tensor* k_pages,
+                          rl_tensor* v_pages, const rl_tensor* k_scale, const rl_tensor* v_scale, void* stream) {
+  return append_impl(k_new, v_new, qo_indptr, block_table, kv_lens, k_pages, v_pages, RL_FP8_E4M3, k_scale, v_scale,
+                     stream);
 }
 
 int rl_attn_merge(const rl_tensor* o_parts, const rl_tensor* lse_parts, const rl_tensor* num_parts, rl_tensor* out,
@@ -893,7 +985,7 @@ int rl_attn_profile_enable(int on) {
 }
 
 int rl_attn_profile_read(int kind, int* launches, double* mean_ms) {
-  if (kind != 0 && kind != 1) return fail(RL_ERR_INVALID_ARG, "kind must be 0 (decode) or 1 (extend)");
+  if (kind < 0 || kind > 2) return fail(RL_ERR_INVALID_ARG, "kind must be 0 (decode), 1 (extend) or 2 (append)");
   if (!launches || !mean_ms) return fail(RL_ERR_INVALID_ARG, "launches and mean_ms must not be NULL");
   std::vector<rl::KernelTimer> ts;
   {

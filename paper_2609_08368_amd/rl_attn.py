@@ -65,6 +65,8 @@ def lib() -> ctypes.CDLL:
         L.rl_attn_extend_ex.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, P, ctypes.POINTER(RlOpts), vp]
         L.rl_attn_decode_fp8.argtypes = [P, P, P, P, P, P, P, ctypes.c_float, P, P, ctypes.POINTER(RlOpts), vp]
         L.rl_attn_extend_fp8.argtypes = [P, P, P, P, P, P, P, P, ctypes.c_float, P, P, ctypes.POINTER(RlOpts), vp]
+        L.rl_attn_append_kv.argtypes = [P, P, P, P, P, P, P, vp]
+        L.rl_attn_append_kv_fp8.argtypes = [P, P, P, P, P, P, P, P, P, vp]
         L.rl_attn_merge.argtypes = [P, P, P, P, P, vp]
         L.rl_attn_last_error.restype = ctypes.c_char_p
         L.rl_attn_check_device_errors.argtypes = [vp]
@@ -80,7 +82,8 @@ def lib() -> ctypes.CDLL:
         L.rl_attn_diag_read_bandwidth.argtypes = [vp, ctypes.c_int64, ctypes.c_int32, dp, vp]
         L.rl_attn_diag_mfma_bf16.argtypes = [ctypes.c_int64, dp, vp]
         for name in ("rl_attn_decode", "rl_attn_extend", "rl_attn_decode_ex", "rl_attn_extend_ex",
-                     "rl_attn_decode_fp8", "rl_attn_extend_fp8", "rl_attn_merge", "rl_attn_check_device_errors", "rl_attn_reserve_workspace",
+                     "rl_attn_decode_fp8", "rl_attn_extend_fp8", "rl_attn_append_kv", "rl_attn_append_kv_fp8",
+                     "rl_attn_merge", "rl_attn_check_device_errors", "rl_attn_reserve_workspace",
                      "rl_attn_profile_enable", "rl_attn_profile_read", "rl_attn_diag_read_bandwidth",
                      "rl_attn_diag_mfma_bf16"):
             getattr(L, name).restype = ctypes.c_int
@@ -218,6 +221,21 @@ def extend_fp8(q, qo_indptr, k_pages, v_pages, k_scale, v_scale, block_table, kv
     return out
 
 
+def append_kv(k_new, v_new, qo_indptr, block_table, kv_lens, k_pages, v_pages, stream=None):
+    """``rl_attn_append_kv``: writes the new rows into ``k_pages``/``v_pages`` (in place)."""
+    _check(lib().rl_attn_append_kv(_ref(view(k_new)), _ref(view(v_new)), _ref(view(qo_indptr)),
+                                   _ref(view(block_table)), _ref(view(kv_lens)), _ref(view(k_pages)),
+                                   _ref(view(v_pages)), _stream(stream)))
+
+
+def append_kv_fp8(k_new, v_new, qo_indptr, block_table, kv_lens, k_pages, v_pages, k_scale, v_scale, stream=None):
+    """``rl_attn_append_kv_fp8``: bf16 rows quantised into ``torch.float8_e4m3fn`` pages (in place)."""
+    _check(lib().rl_attn_append_kv_fp8(_ref(view(k_new)), _ref(view(v_new)), _ref(view(qo_indptr)),
+                                       _ref(view(block_table)), _ref(view(kv_lens)), _ref(view(k_pages)),
+                                       _ref(view(v_pages)), _ref(view(k_scale)), _ref(view(v_scale)),
+                                       _stream(stream)))
+
+
 def merge(o_parts, lse_parts, num_parts, out=None, lse=None, stream=None):
     """``rl_attn_merge``: log-sum-exp merge of partial results."""
     n, _, h, d = o_parts.shape
@@ -241,10 +259,11 @@ def profile_enable(on: bool = True):
 
 
 def profile_read(kind: str):
-    """(launches, mean ms) of the main kernel timed since the last read; kind 'decode' or 'extend'."""
+    """(launches, mean ms) of the main kernel timed since the last read; kind 'decode', 'extend' or 'append'."""
     n = ctypes.c_int()
     ms = ctypes.c_double()
-    _check(lib().rl_attn_profile_read({"decode": 0, "extend": 1}[kind], ctypes.byref(n), ctypes.byref(ms)))
+    _check(lib().rl_attn_profile_read({"decode": 0, "extend": 1, "append": 2}[kind], ctypes.byref(n),
+                                      ctypes.byref(ms)))
     return n.value, ms.value
 
 

@@ -221,3 +221,32 @@ def test_fp8_extend_validation():
     rc = ra.lib().rl_attn_extend_fp8(r(q), r(indptr), r(fake([20, 16, 2, 128], ra.RL_BF16)), r(k), r(ks), r(ks),
                                      r(bt), r(kv), ctypes.c_float(1.0), r(out), None, None, None)
     assert ra.STATUS[rc] == "RL_ERR_DTYPE"
+
+
+def test_append_validation():
+    r = ctypes.byref
+    lib = ra.lib()
+    B, T = 3, 10
+    kn = fake([T, 2, 128], ra.RL_BF16)
+    kp = fake([20, 16, 2, 128], ra.RL_BF16)
+    bt = fake([B, 4], ra.RL_I32)
+    kv = fake([B], ra.RL_I32)
+    ind = fake([B + 1], ra.RL_I32)
+
+    def call(k_new=kn, v_new=kn, indptr=ind, pages=kp):
+        return ra.STATUS[lib.rl_attn_append_kv(r(k_new), r(v_new), r(indptr), r(bt), r(kv), r(pages), r(pages), None)]
+
+    assert call(v_new=fake([T, 2, 64], ra.RL_BF16)) == "RL_ERR_SHAPE"
+    assert call(k_new=fake([T, 2, 128], ra.RL_F32), v_new=fake([T, 2, 128], ra.RL_F32)) == "RL_ERR_DTYPE"
+    assert call(k_new=fake([T, 4, 128], ra.RL_BF16), v_new=fake([T, 4, 128], ra.RL_BF16)) == "RL_ERR_SHAPE"
+    assert "KV heads" in ra.last_error()
+    assert call(indptr=fake([B], ra.RL_I32)) == "RL_ERR_SHAPE" and "qo_indptr" in ra.last_error()
+    assert call(pages=fake([20, 16, 2, 128], ra.RL_FP8_E4M3)) == "RL_ERR_DTYPE"
+    f8 = fake([20, 16, 2, 128], ra.RL_FP8_E4M3)
+    sc = fake([2], ra.RL_F32)
+    rc = lib.rl_attn_append_kv_fp8(r(kn), r(kn), r(ind), r(bt), r(kv), r(f8), r(f8), r(sc), r(fake([3], ra.RL_F32)), None)
+    assert ra.STATUS[rc] == "RL_ERR_SHAPE" and "v_scale" in ra.last_error()
+    rc = lib.rl_attn_append_kv_fp8(r(kn), r(kn), r(ind), r(bt), r(kv), r(kp), r(kp), r(sc), r(sc), None)
+    assert ra.STATUS[rc] == "RL_ERR_DTYPE"
+    empty = fake([0, 2, 128], ra.RL_BF16)
+    assert call(k_new=empty, v_new=empty) == "RL_OK"
