@@ -381,6 +381,48 @@ def append_study(steps: int, warmup: int, w_ext, w_dec) -> dict:
     return res
 
 
+def mtp_study(steps: int, warmup: int, w, t, single_ms: float) -> dict:
+    """Multi-token decode (n query tokens per sequence, as when verifying multi-token-prediction
+    drafts) on the ragged batch's pages: the KV bytes are read once for all n tokens."""
+    import torch
+
+    from paper_2609_08368_amd import rl_attn as ra
+
+    dev = torch.device("cuda:0")
+    res = {"workload": "ragged 64K decode batch, bf16 pages, n query tokens per sequence (the last n keys)"}
+    for n in (2, 4, 8):
+        g = torch.Generator(device=dev)
+        g.manual_seed(900 + n)
+        q = torch.randn((w.batch, n, w.hq, 128), generator=g, device=dev).to(torch.bfloat16)
+        out = torch.empty_like(q)
+
+        def fn():
+            ra.decode(q, t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out)
+
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        ra.profile_read("decode")
+        ra.profile_enable(True)
+        stream = torch.cuda.current_stream()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(steps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        ra.profile_enable(False)
+        _, kern_ms = ra.profile_read("decode")
+        ms = a.elapsed_time(b) / steps
+        gbps = w.kv_bytes() / (ms * 1e-3) / 1e9
+        res[f"n{n}"] = {"ms_mean": round(ms, 4), "kernel_ms": round(kern_ms, 4), "kv_GBps": round(gbps, 2),
+                        "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
+                        "query_tokens_per_s": round(w.batch * n / (ms * 1e-3), 1),
+                        "time_vs_single_token": round(ms / single_ms, 3)}
+    log(f"multi-token decode: {res}")
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -551,6 +593,7 @@ def main():
     torch.cuda.empty_cache()
     result["deterministic_decode"] = deterministic_study(args.steps, args.warmup, w_dec, t_dec,
                                                          mean["decode_ragged"])
+    result["multi_token_decode"] = mtp_study(args.steps, args.warmup, w_dec, t_dec, mean["decode_ragged"])
     result["kv_append"] = append_study(args.steps, args.warmup, w_ext, w_dec)
     result["fp8_kv"] = fp8_study(args.steps, args.warmup, w_dec, w_ext, mean["decode_ragged"],
                                  mean["extend_multiturn"])

@@ -113,7 +113,14 @@ typedef struct {
 } rl_attn_opts;
 
 /* Batched decode (paper: batched generation by the rollout engines).
- *   q           [B, Hq, 128] bf16
+ *   q           [B, Hq, 128] bf16, or [B, n, Hq, 128] for n query tokens per
+ *               sequence (1 <= n <= 64; multi-token decode, e.g. verifying the
+ *               draft tokens of multi-token prediction, which the case study's
+ *               rollout engines use: section "Case Study", subsection
+ *               "Configuration"). The n tokens are the last n of the sequence
+ *               (their K/V already in the pages) and token i sees keys
+ *               t <= seq_lens[b] - n + i; out is [B, n, Hq, 128] and lse_out
+ *               [B, n, Hq]. The _fp8 call accepts the same shapes.
  *   k_pages     [num_pages, P, Hkv, 128] bf16
  *   v_pages     same shape and dtype as k_pages
  *   block_table [B, max_pages] int32 (entries past ceil(seq_lens[b]/P) are never read)
@@ -228,7 +235,8 @@ int rl_attn_check_device_errors(void* stream);
  * calls (e.g. under stream capture) need no allocation. */
 int rl_attn_reserve_workspace(size_t bytes, void* stream);
 
-/* Workspace bytes a decode / extend call with these sizes may need. */
+/* Workspace bytes a decode / extend call with these sizes may need (for a
+ * decode with n query tokens per sequence pass num_q_heads = n * Hq). */
 size_t rl_attn_decode_workspace_size(int64_t batch, int64_t num_q_heads, int64_t num_kv_heads,
                                      int64_t max_pages, int64_t page_size);
 size_t rl_attn_extend_workspace_size(int64_t batch, int64_t total_q, int64_t num_q_heads,

@@ -551,10 +551,10 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
       }
       if (a.lse && grp == 0) a.lse[(int64_t)b * a.lse_sb + (int64_t)h * a.lse_sh] = res.lse;
     } else {
-      float* pp = a.ws.part_o + ((int64_t)slot * a.Hq + h) * kHeadDim + 4 * grp;
+      float* pp = a.ws.part_o + ((int64_t)slot * a.Hv + h) * kHeadDim + 4 * grp;
 #pragma unroll
       for (int j = 0; j < 8; ++j) *reinterpret_cast<f32x4*>(pp + 16 * j) = o[j] * inv;
-      if (grp == 0) a.ws.part_lse[(int64_t)slot * a.Hq + h] = res.lse;
+      if (grp == 0) a.ws.part_lse[(int64_t)slot * a.Hv + h] = res.lse;
     }
   }
   });
@@ -634,10 +634,10 @@ __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
       }
       if (a.lse && c16 == 0) a.lse[(int64_t)b * a.lse_sb + (int64_t)h * a.lse_sh] = res.lse;
     } else {
-      float* pp = a.ws.part_o + ((int64_t)slot * a.Hq + h) * kHeadDim + c16 * 8;
+      float* pp = a.ws.part_o + ((int64_t)slot * a.Hv + h) * kHeadDim + c16 * 8;
 #pragma unroll
       for (int i = 0; i < 8; ++i) pp[i] = acc[i] * inv;
-      if (c16 == 0) a.ws.part_lse[(int64_t)slot * a.Hq + h] = res.lse;
+      if (c16 == 0) a.ws.part_lse[(int64_t)slot * a.Hv + h] = res.lse;
     }
   }
   });
@@ -645,10 +645,81 @@ __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
   if (bad_scale) atomicOr(a.ws.err, kErrScale);
 }
 
+// Multi-token decode (n_tok > 1, e.g. verifying multi-token-prediction
+// drafts): the n_tok * R rows (query token, query head) of one KV head share
+// every key, so one workgroup computes up to 128 of them with the LDS-staged
+// tile routine (K and V read once per workgroup), over the same equal-work
+// pieces as single-token decode. Token i of a sequence of length L sees keys
+// t <= L - n_tok + i. Pieces start on 32-key tiles; the routine's steps start
+// on 64-key boundaries, so a piece's first step masks the keys before it.
+constexpr int kMultiWaves = 4;          // waves per multi-token workgroup: 128 rows
+
+template <bool kFp8>
+__global__ __launch_bounds__(kMultiWaves * 64, 2) void decode_multi_kernel(DecodeArgs a) {
+  __shared__ TileLds lds;
+  const int rows = a.n_tok * a.R;
+  const int nrb = (rows + kMultiWaves * kWaveRows - 1) / (kMultiWaves * kWaveRows);
+  const int nch = a.Hkv * nrb;                  // workgroups per worker
+  const int worker = blockIdx.x / nch;
+  const int rem = blockIdx.x - worker * nch;
+  const int g = rem % a.Hkv, rb = rem / a.Hkv;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int rr = rb * kMultiWaves * kWaveRows + wave * kWaveRows + (lane & 31);
+  const bool row_ok = rr < rows;
+  const int tok = row_ok ? rr / a.R : 0;
+  const int head = g * a.R + (row_ok ? rr - tok * a.R : 0);
+  int bad = 0, bad_short = 0, bad_scale = 0;
+  const KvScales dq = kv_scales<kFp8>(a.kv, g, &bad_scale);
+  const float scale = a.scale * dq.k;
+
+  for_each_piece(a, worker, [&](int b, int t_begin, int t_end, int slot) {
+    const int L = a.ws.seqs[b].z;
+    if (L < a.n_tok) bad_short = 1;          // the query tokens must be in the cache
+    const int limit = L - a.n_tok + tok;
+    bf16x8 qv[8];
+    load_q_operand((const __bf16*)a.q + (int64_t)b * a.q_sb + (int64_t)tok * a.q_st + (int64_t)head * a.q_sh, row_ok,
+                   qv);
+    f32x16 o[4];
+#pragma unroll
+    for (int jd = 0; jd < 4; ++jd)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[jd][e] = 0.f;
+    float m_run = kNegInf, l_run = 0.f;
+    const int t_lo = t_begin & ~(kKeys - 1);
+    // keys below L - n + 1 are visible to every token (t_full may not pass the
+    // piece's end: the routine masks keys at or past t_hi only from t_full on)
+    const int t_full = min(L - a.n_tok + 1, t_end);
+    tile_attend<kMultiWaves, false, kFp8>(a.kv, scale, a.kv.bt + (int64_t)b * a.kv.bt_sb, g, t_lo, t_end, t_full,
+                                          limit, qv, lds, o, m_run, l_run, bad, t_begin);
+    const HeadResult res = finish(m_run, sum_l32(l_run));
+    if (row_ok) {
+      const float inv = res.inv * dq.v;
+      if (slot < 0) {
+        const int64_t oo = (int64_t)b * a.out_sb + (int64_t)tok * a.out_st + (int64_t)head * a.out_sh;
+        if (a.out_f32)
+          store_o_row((float*)a.out + oo, o, inv);
+        else
+          store_o_row((__bf16*)a.out + oo, o, inv);
+        if (a.lse && lane < 32)
+          a.lse[(int64_t)b * a.lse_sb + (int64_t)tok * a.lse_st + (int64_t)head * a.lse_sh] = res.lse;
+      } else {
+        const int64_t row = (int64_t)slot * a.Hv + (int64_t)tok * a.Hq + head;
+        store_o_row(a.ws.part_o + row * kHeadDim, o, inv);
+        if (lane < 32) a.ws.part_lse[row] = res.lse;
+      }
+    }
+    __syncthreads();  // the LDS tiles are reused by the next piece
+  });
+  if (bad) atomicOr(a.ws.err, kErrPage);
+  if (bad_short) atomicOr(a.ws.err, kErrKvShort);
+  if (bad_scale) atomicOr(a.ws.err, kErrScale);
+}
+
 // Group-prefix pass: one workgroup per (shared item, KV head) computes the
 // shared keys of a sub-group once for all its members' query rows (row r ->
-// member r / R, query head r % R), reading each shared page once, and writes
-// one partial per member into that member's slot for this split.
+// member r / (n R), then query token, then query head), reading each shared
+// page once, and writes one partial per member into that member's slot for
+// this split.
 constexpr int kPrefixWaves = 4;         // waves per group-prefix workgroup: 128 member rows
 
 template <bool kFp8>
@@ -665,13 +736,19 @@ __global__ __launch_bounds__(kPrefixWaves * 64, 2) void prefix_kernel(DecodeArgs
     const int4 info = a.ws.sgroups[sg];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = wave * kWaveRows + (lane & 31);
-    const int member = r / a.R, hi = r - member * a.R;
+    const int rows_m = a.n_tok * a.R;               // rows of one member
+    const int member = r / rows_m, rm = r - member * rows_m;
+    const int tok = rm / a.R, hi = rm - tok * a.R;
     const bool row_ok = member < info.y;
     const int b = a.ws.sg_members[sg * a.group_cap + (row_ok ? member : 0)];
     const int head = g * a.R + hi;
+    // token tok of a member of length L sees keys t <= L - n + tok (with one
+    // token the shared keys are all visible)
+    const int limit = a.n_tok == 1 ? t1 - 1 : a.ws.seqs[b].z - a.n_tok + tok;
 
     bf16x8 qv[8];
-    load_q_operand((const __bf16*)a.q + (int64_t)b * a.q_sb + (int64_t)head * a.q_sh, row_ok, qv);
+    load_q_operand((const __bf16*)a.q + (int64_t)b * a.q_sb + (int64_t)tok * a.q_st + (int64_t)head * a.q_sh, row_ok,
+                   qv);
     f32x16 o[4];
 #pragma unroll
     for (int jd = 0; jd < 4; ++jd)
@@ -680,14 +757,15 @@ __global__ __launch_bounds__(kPrefixWaves * 64, 2) void prefix_kernel(DecodeArgs
     float m_run = kNegInf, l_run = 0.f;
     int bad = 0, bad_scale = 0;
     const KvScales dq = kv_scales<kFp8>(a.kv, g, &bad_scale);
-    tile_attend<kPrefixWaves, false, kFp8>(a.kv, a.scale * dq.k, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g, t0, t1, t1, t1 - 1,
-                                           qv, lds, o, m_run, l_run, bad);
+    tile_attend<kPrefixWaves, false, kFp8>(a.kv, a.scale * dq.k, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g, t0, t1,
+                                           a.n_tok == 1 ? t1 : t0, limit, qv, lds, o, m_run, l_run, bad);
     const HeadResult res = finish(m_run, sum_l32(l_run));
     if (row_ok) {
       const int slot = a.ws.base[b] + split;
       if (slot < a.max_slots) {
-        store_o_row(a.ws.part_o + ((int64_t)slot * a.Hq + head) * kHeadDim, o, res.inv * dq.v);
-        if (lane < 32) a.ws.part_lse[(int64_t)slot * a.Hq + head] = res.lse;
+        const int64_t row = (int64_t)slot * a.Hv + (int64_t)tok * a.Hq + head;
+        store_o_row(a.ws.part_o + row * kHeadDim, o, res.inv * dq.v);
+        if (lane < 32) a.ws.part_lse[row] = res.lse;
       }
     }
     if (bad) atomicOr(a.ws.err, kErrPage);
@@ -742,27 +820,30 @@ __device__ __forceinline__ void merge_parts(const float* o_base, int64_t o_step,
 }
 
 __global__ __launch_bounds__(64) void combine_kernel(DecodeArgs a) {
-  const int b = blockIdx.x / a.Hq;
-  const int h = blockIdx.x - b * a.Hq;
+  // one (sequence, row) per wave; row hv = token * Hq + query head
+  const int b = blockIdx.x / a.Hv;
+  const int hv = blockIdx.x - b * a.Hv;
+  const int tok = hv / a.Hq, h = hv - tok * a.Hq;
   const int n = a.ws.nparts[b];
   if (n == 0) return;     // written directly by its only piece
   float r[2] = {0.f, 0.f}, lse_v = kNegInf;   // an empty sequence (n < 0): zeros, -inf
   if (n > 0) {
     const int base = a.ws.base[b];
-    merge_parts(a.ws.part_o + ((int64_t)base * a.Hq + h) * kHeadDim, (int64_t)a.Hq * kHeadDim,
-                a.ws.part_lse + (int64_t)base * a.Hq + h, a.Hq, n, r, &lse_v);
+    merge_parts(a.ws.part_o + ((int64_t)base * a.Hv + hv) * kHeadDim, (int64_t)a.Hv * kHeadDim,
+                a.ws.part_lse + (int64_t)base * a.Hv + hv, a.Hv, n, r, &lse_v);
   }
   const int lane = threadIdx.x;
+  const int64_t oo = (int64_t)b * a.out_sb + (int64_t)tok * a.out_st + (int64_t)h * a.out_sh + 2 * lane;
   if (a.out_f32) {
-    float* op = (float*)a.out + (int64_t)b * a.out_sb + (int64_t)h * a.out_sh + 2 * lane;
+    float* op = (float*)a.out + oo;
     op[0] = r[0];
     op[1] = r[1];
   } else {
-    __bf16* op = (__bf16*)a.out + (int64_t)b * a.out_sb + (int64_t)h * a.out_sh + 2 * lane;
+    __bf16* op = (__bf16*)a.out + oo;
     op[0] = (__bf16)r[0];
     op[1] = (__bf16)r[1];
   }
-  if (a.lse && lane == 0) a.lse[(int64_t)b * a.lse_sb + (int64_t)h * a.lse_sh] = lse_v;
+  if (a.lse && lane == 0) a.lse[(int64_t)b * a.lse_sb + (int64_t)tok * a.lse_st + (int64_t)h * a.lse_sh] = lse_v;
 }
 
 __global__ __launch_bounds__(64) void merge_kernel(MergeArgs a) {
@@ -791,7 +872,11 @@ void launch_decode_kernels(const DecodeArgs& a, hipStream_t stream, KernelTimer*
   const unsigned per_item = a.R == 1 ? a.Hkv : a.Hkv * ((a.R + 15) / 16);
   if (a.group_cap >= 2) prefix_kernel<kFp8><<<(unsigned)a.prefix_grid, kPrefixWaves * 64, 0, stream>>>(a);
   if (timer) (void)hipEventRecord(timer->start, stream);
-  if (a.R == 1) {
+  if (a.n_tok > 1) {
+    const int rows = a.n_tok * a.R;
+    const int64_t nch = (int64_t)a.Hkv * ((rows + kMultiWaves * kWaveRows - 1) / (kMultiWaves * kWaveRows));
+    decode_multi_kernel<kFp8><<<(unsigned)(a.max_workers * nch), kMultiWaves * 64, 0, stream>>>(a);
+  } else if (a.R == 1) {
     decode_valu_kernel<kFp8><<<(unsigned)a.max_workers * per_item, 64, 0, stream>>>(a);
   } else {
     const unsigned nch = per_item / a.item_waves;
@@ -803,8 +888,11 @@ void launch_decode_kernels(const DecodeArgs& a, hipStream_t stream, KernelTimer*
 }
 
 template <bool kFp8>
-int workers_per_cu_of(int R, int Hkv, int item_waves) {
+int workers_per_cu_of(int R, int Hkv, int item_waves, int n_tok) {
   int blocks = 0;
+  // multi-token decode: one worker per CU; a worker's Hkv x row-block
+  // workgroups then run in equal rounds
+  if (n_tok > 1) return 1;
   if (R == 1) {
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_valu_kernel<kFp8>, 64, 0) != hipSuccess) blocks = 0;
     return blocks / Hkv > 1 ? blocks / Hkv : 1;
@@ -824,12 +912,12 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream, KernelTimer* t
     launch_decode_kernels<true>(a, stream, timer);
   else
     launch_decode_kernels<false>(a, stream, timer);
-  combine_kernel<<<(unsigned)(a.B * a.Hq), 64, 0, stream>>>(a);
+  combine_kernel<<<(unsigned)((int64_t)a.B * a.Hv), 64, 0, stream>>>(a);
   return hipGetLastError();
 }
 
-int decode_workers_per_cu(int R, int Hkv, int item_waves, bool fp8) {
-  return fp8 ? workers_per_cu_of<true>(R, Hkv, item_waves) : workers_per_cu_of<false>(R, Hkv, item_waves);
+int decode_workers_per_cu(int R, int Hkv, int item_waves, bool fp8, int n_tok) {
+  return fp8 ? workers_per_cu_of<true>(R, Hkv, item_waves, n_tok) : workers_per_cu_of<false>(R, Hkv, item_waves, n_tok);
 }
 
 hipError_t launch_merge(const MergeArgs& a, hipStream_t stream) {

@@ -26,12 +26,19 @@ struct SeqRange {
 __device__ __forceinline__ SeqRange seq_range(const ExtendArgs& a, int b, int* bad) {
   const int max_tokens = a.kv.max_pages * a.kv.page_size;
   if (a.decode_rows) {
+    // decode: sequence b owns rows b * n .. b * n + n - 1, its last n keys
+    const int n = a.decode_rows;
     int kv = a.kv_lens[(int64_t)b * a.kv_lens_s];
     if (kv < 0 || kv > max_tokens) {
       *bad |= kErrLen;
       kv = kv < 0 ? 0 : max_tokens;
     }
-    return {b, kv > 0 ? 1 : 0, kv};
+    if (kv == 0) return {b * n, 0, 0};
+    if (kv < n) {
+      *bad |= kErrKvShort;
+      kv = n <= max_tokens ? n : max_tokens;
+    }
+    return {b * n, n, kv};
   }
   int q0 = a.qo_indptr[(int64_t)b * a.indptr_s];
   int q1 = a.qo_indptr[(int64_t)(b + 1) * a.indptr_s];
@@ -62,18 +69,21 @@ __global__ __launch_bounds__(1024) void plan_extend_kernel(ExtendArgs a) {
   int bad = 0;
   if (a.decode_rows) {
     // decode rows of empty sequences have no work unit: out = 0, lse = -inf
-    for (int i = tid; i < a.B * a.Hq; i += blockDim.x) {
-      const int b = i / a.Hq, h = i - b * a.Hq;
+    const int per_seq = a.decode_rows * a.Hq;
+    for (int i = tid; i < a.B * per_seq; i += blockDim.x) {
+      const int b = i / per_seq, rest = i - b * per_seq;
+      const int64_t row = (int64_t)b * a.decode_rows + rest / a.Hq;
+      const int h = rest % a.Hq;
       int dummy = 0;
       if (seq_range(a, b, &dummy).n != 0) continue;
       if (a.out_f32) {
-        float4* op = reinterpret_cast<float4*>((float*)a.out + b * a.out_st + (int64_t)h * a.out_sh);
+        float4* op = reinterpret_cast<float4*>((float*)a.out + row * a.out_st + (int64_t)h * a.out_sh);
         for (int c = 0; c < kHeadDim / 4; ++c) op[c] = make_float4(0.f, 0.f, 0.f, 0.f);
       } else {
-        uint4* op = reinterpret_cast<uint4*>((__bf16*)a.out + b * a.out_st + (int64_t)h * a.out_sh);
+        uint4* op = reinterpret_cast<uint4*>((__bf16*)a.out + row * a.out_st + (int64_t)h * a.out_sh);
         for (int c = 0; c < kHeadDim / 8; ++c) op[c] = make_uint4(0u, 0u, 0u, 0u);
       }
-      if (a.lse) a.lse[b * a.lse_st + (int64_t)h * a.lse_sh] = kNegInf;
+      if (a.lse) a.lse[row * a.lse_st + (int64_t)h * a.lse_sh] = kNegInf;
     }
   }
   const bool sorted = a.B <= kSortMax;

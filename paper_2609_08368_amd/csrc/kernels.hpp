@@ -58,6 +58,14 @@ struct DecodeArgs {
   PagedKV kv;
   const void* q;
   int64_t q_sb, q_sh;
+  // query tokens per sequence (multi-token decode: the sequence's last n_tok
+  // keys are these tokens and token i sees keys t <= L - n_tok + i); token
+  // strides of q, out and lse (unused when n_tok == 1)
+  int n_tok;
+  int64_t q_st, out_st, lse_st;
+  // rows of the partial buffers and of the combine per sequence: n_tok * Hq,
+  // row i * Hq + h for token i, query head h
+  int Hv;
   const int* lens;
   int64_t lens_s;
   int B, Hq, Hkv, R;
@@ -72,7 +80,7 @@ struct DecodeArgs {
   int max_items;          // capacity of the shared item list
   int max_workers;        // workers the private pass may use (its grid / workgroups per worker)
   int max_slots;          // capacity of the partial buffers
-  int group_cap;          // members per sub-group (128 query rows / R), 0 = no prefix sharing
+  int group_cap;          // members per sub-group (128 query rows / (n_tok * R)), 0 = no prefix sharing
   int prefix_grid;        // workgroups of the group-prefix pass (grid-stride over its work)
   int item_waves;         // waves per decode workgroup: a divisor of Hkv * ceil(R / 16), at most 8
   DecodePlanWs ws;
@@ -102,9 +110,10 @@ struct ExtendArgs {
   float* lse;
   int64_t lse_st, lse_sh;
   int max_items;
-  // 1: decode through the extend kernel: sequence b owns query row b alone
-  // (one row if kv_lens[b] > 0, none otherwise; qo_indptr is not read), and
-  // the rows of empty sequences are written as zeros with lse = -inf
+  // n > 0: decode through the extend kernel: sequence b owns query rows
+  // b n .. b n + n - 1, its last n keys (none if kv_lens[b] == 0; qo_indptr is
+  // not read), and the rows of empty sequences are written as zeros with
+  // lse = -inf
   int decode_rows;
   ExtendPlanWs ws;
 };
@@ -159,7 +168,7 @@ double diag_mfma_flops(int iters, int cus);
 
 // Workers of the private decode pass that are resident on one CU at a time
 // (from the kernel's occupancy; a worker is one workgroup per wave group).
-int decode_workers_per_cu(int R, int Hkv, int item_waves, bool fp8);
+int decode_workers_per_cu(int R, int Hkv, int item_waves, bool fp8, int n_tok);
 hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream, KernelTimer* timer);
 hipError_t launch_merge(const MergeArgs& a, hipStream_t stream);
 hipError_t launch_append(const AppendArgs& a, hipStream_t stream, KernelTimer* timer);

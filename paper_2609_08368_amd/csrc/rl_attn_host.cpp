@@ -282,31 +282,35 @@ int target_items_for(int64_t Hq, int64_t Hkv, int cus) {
 }
 
 // workers of the private pass resident on one CU (cached per shape)
-int workers_per_cu(int64_t Hq, int64_t Hkv, bool fp8) {
+int workers_per_cu(int64_t Hq, int64_t Hkv, bool fp8, int n_tok) {
   if (env().workers_per_cu > 0) return env().workers_per_cu;
   static std::mutex mu;
-  static std::map<std::tuple<int64_t, int64_t, bool>, int> cache;
+  static std::map<std::tuple<int64_t, int64_t, bool, int>, int> cache;
   std::lock_guard<std::mutex> lk(mu);
-  auto it = cache.find({Hq, Hkv, fp8});
+  auto it = cache.find({Hq, Hkv, fp8, n_tok});
   if (it != cache.end()) return it->second;
   const int R = (int)(Hq / std::max<int64_t>(1, Hkv));
-  const int n = rl::decode_workers_per_cu(R, (int)Hkv, decode_item_waves(Hq, Hkv), fp8);
-  cache[{Hq, Hkv, fp8}] = n;
+  const int n = rl::decode_workers_per_cu(R, (int)Hkv, decode_item_waves(Hq, Hkv), fp8, n_tok);
+  cache[{Hq, Hkv, fp8, n_tok}] = n;
   return n;
 }
 
+// n_tok query tokens per sequence: partial rows and group sizes count n_tok * Hq
+// rows per sequence (the layout of (Hq, n_tok) is at most that of (n_tok * Hq, 1))
 DecodeLayout decode_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t max_pages, int64_t P, int split, int cus,
-                           bool prefix_share, bool fp8) {
+                           bool prefix_share, bool fp8, int n_tok = 1) {
   DecodeLayout L{};
   const int64_t R = Hq / std::max<int64_t>(1, Hkv);
+  const int64_t rows_kv = R * n_tok;              // query rows of one KV head
+  const int64_t Hv = Hq * n_tok;
   const int64_t max_tokens = max_pages * P;
   const int64_t T = split > 0 ? B * std::max<int64_t>(1, (max_tokens + split - 1) / split)
                               : (int64_t)target_items_for(Hq, Hkv, cus);
-  const int64_t workers = split > 0 ? T : (int64_t)cus * workers_per_cu(Hq, Hkv, fp8);
+  const int64_t workers = split > 0 ? T : (int64_t)cus * workers_per_cu(Hq, Hkv, fp8, n_tok);
   L.max_items = (int)std::min<int64_t>(T + B, INT32_MAX / 2);
   L.max_workers = (int)std::min<int64_t>(std::max<int64_t>(1, workers), INT32_MAX / 64);
   L.max_slots = (int)std::min<int64_t>(L.max_workers + T + 2 * B, INT32_MAX / 2);
-  L.group_cap = (prefix_share && R <= 64) ? (int)(128 / R) : 0;
+  L.group_cap = (prefix_share && rows_kv <= 64) ? (int)(128 / rows_kv) : 0;
   size_t off = 256;  // header
   L.off_nparts = off;
   off += align256(B * 4);
@@ -323,9 +327,9 @@ DecodeLayout decode_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t max_pages
   L.off_members = off;
   off += align256((size_t)B * std::max(1, L.group_cap) * 4);
   L.off_po = off;
-  off += align256((size_t)L.max_slots * Hq * 128 * 4);
+  off += align256((size_t)L.max_slots * Hv * 128 * 4);
   L.off_pl = off;
-  off += align256((size_t)L.max_slots * Hq * 4);
+  off += align256((size_t)L.max_slots * Hv * 4);
   L.total = off;
   return L;
 }
@@ -411,10 +415,10 @@ int fill_paged(const rl_tensor* k, const rl_tensor* v, const rl_tensor* bt, int6
 }
 
 int check_out(const rl_tensor* out, const rl_tensor* q, const char* name, int* is_f32) {
-  RL_TRY(check_view(out, name, 3));
+  RL_TRY(check_view(out, name, q->ndim));
   if (out->dtype != RL_BF16 && out->dtype != RL_F32)
     return fail(RL_ERR_DTYPE, "%s must be bf16 or f32 (got %s)", name, dtype_name(out->dtype));
-  for (int i = 0; i < 3; ++i)
+  for (int i = 0; i < q->ndim; ++i)
     if (out->shape[i] != q->shape[i]) return fail(RL_ERR_SHAPE, "%s shape must equal q's (dim %d)", name, i);
   RL_TRY(check_rows128(out, name));
   RL_TRY(check_data(out, name));
@@ -422,11 +426,13 @@ int check_out(const rl_tensor* out, const rl_tensor* q, const char* name, int* i
   return RL_OK;
 }
 
-int check_lse(const rl_tensor* lse, int64_t rows, int64_t heads) {
+int check_lse(const rl_tensor* lse, int64_t rows, int64_t heads, int64_t tokens = 0) {
   if (!lse) return RL_OK;
-  RL_TRY(check_view(lse, "lse_out", 2));
+  RL_TRY(check_view(lse, "lse_out", tokens ? 3 : 2));
   RL_TRY(check_dtype(lse, "lse_out", RL_F32));
-  if (lse->shape[0] != rows || lse->shape[1] != heads) return fail(RL_ERR_SHAPE, "lse_out shape mismatch");
+  if (tokens ? (lse->shape[0] != rows || lse->shape[1] != tokens || lse->shape[2] != heads)
+             : (lse->shape[0] != rows || lse->shape[1] != heads))
+    return fail(RL_ERR_SHAPE, "lse_out shape mismatch");
   RL_TRY(check_data(lse, "lse_out"));
   return RL_OK;
 }
@@ -488,10 +494,16 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   Opts o;
   RL_TRY(read_opts(opts, &o));
   RL_TRY(check_scale(scale));
-  RL_TRY(check_view(q, "q", 3));
+  if (!q) return fail(RL_ERR_INVALID_ARG, "q is NULL");
+  if (q->ndim != 3 && q->ndim != 4)
+    return fail(RL_ERR_SHAPE, "q must have 3 dimensions, or 4 for several query tokens (got %d)", q->ndim);
+  RL_TRY(check_view(q, "q", q->ndim));
   RL_TRY(check_dtype(q, "q", RL_BF16));
   RL_TRY(check_rows128(q, "q"));
-  const int64_t B = q->shape[0], Hq = q->shape[1];
+  const bool multi = q->ndim == 4;
+  const int64_t B = q->shape[0], Hq = q->shape[q->ndim - 2];
+  const int64_t n_tok = multi ? q->shape[1] : 1;
+  if (n_tok < 1 || n_tok > 64) return fail(RL_ERR_UNSUPPORTED, "query tokens per sequence must be in [1, 64]");
   rl::DecodeArgs a{};
   RL_TRY(fill_paged(k_pages, v_pages, block_table, B, kv_dtype, k_scale, v_scale, &a.kv));
   const int64_t Hkv = k_pages->shape[2];
@@ -503,39 +515,49 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   if (seq_lens->shape[0] != B) return fail(RL_ERR_SHAPE, "seq_lens.shape[0] != batch");
   int is_f32 = 0;
   RL_TRY(check_out(out, q, "out", &is_f32));
-  RL_TRY(check_lse(lse_out, B, Hq));
+  RL_TRY(check_lse(lse_out, B, Hq, multi ? n_tok : 0));
   if (B > (1 << 22) || Hq > 4096) return fail(RL_ERR_UNSUPPORTED, "batch or head count too large");
   RL_TRY(check_data(q, "q"));
   RL_TRY(check_data(seq_lens, "seq_lens"));
   if (B == 0) return RL_OK;
+  // token strides (dimension 1 of a 4-D q / out, of a 3-D lse)
+  const int64_t q_st = multi ? q->strides[1] : 0, out_st = multi ? out->strides[1] : 0;
+  const int64_t lse_st = (multi && lse_out) ? lse_out->strides[1] : 0;
+  const int hd = q->ndim - 2;                      // head dimension index of q / out
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (o.deterministic) {
     // one extend row per sequence: the same kernel and per-row arithmetic as
     // extend, with no split of the keys, so the result of a sequence does not
     // depend on the rest of the batch and equals extend's bitwise
+    // extend rows are (sequence, token) pairs in one run: token dimensions
+    // must merge with the batch dimension
+    if (multi && (q->strides[0] != n_tok * q_st || out->strides[0] != n_tok * out_st ||
+                  (lse_out && lse_out->strides[0] != n_tok * lse_st)))
+      return fail(RL_ERR_UNSUPPORTED,
+                  "deterministic multi-token decode needs q, out and lse_out with batch stride = tokens x token stride");
     rl::ExtendArgs e{};
     e.kv = a.kv;
     e.q = q->data;
-    e.q_st = q->strides[0];
-    e.q_sh = q->strides[1];
+    e.q_st = multi ? q_st : q->strides[0];
+    e.q_sh = q->strides[hd];
     e.qo_indptr = nullptr;
     e.kv_lens = static_cast<const int*>(seq_lens->data);
     e.kv_lens_s = seq_lens->strides[0];
     e.B = (int)B;
-    e.total_q = (int)B;
+    e.total_q = (int)(B * n_tok);
     e.Hq = (int)Hq;
     e.Hkv = (int)Hkv;
     e.R = (int)(Hq / Hkv);
     e.scale = scale;
     e.out = out->data;
     e.out_f32 = is_f32;
-    e.out_st = out->strides[0];
-    e.out_sh = out->strides[1];
+    e.out_st = multi ? out_st : out->strides[0];
+    e.out_sh = out->strides[hd];
     e.lse = lse_out ? static_cast<float*>(lse_out->data) : nullptr;
-    e.lse_st = lse_out ? lse_out->strides[0] : 0;
-    e.lse_sh = lse_out ? lse_out->strides[1] : 0;
-    e.decode_rows = 1;
+    e.lse_st = lse_out ? (multi ? lse_st : lse_out->strides[0]) : 0;
+    e.lse_sh = lse_out ? lse_out->strides[multi ? 2 : 1] : 0;
+    e.decode_rows = (int)n_tok;
     return run_extend(e, st, 0);
   }
   int dev = 0;
@@ -543,13 +565,18 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   const int cus = device_cus(dev);
   const DecodeLayout lay = decode_layout(B, Hq, Hkv, a.kv.max_pages, a.kv.page_size, o.split_tokens, cus,
-                                         o.prefix_share == RL_PREFIX_AUTO, kv_dtype == RL_FP8_E4M3);
+                                         o.prefix_share == RL_PREFIX_AUTO, kv_dtype == RL_FP8_E4M3, (int)n_tok);
   Workspace* w = nullptr;
   RL_TRY(acquire_ws(st, lay.total, &w));
   char* base = static_cast<char*>(w->ptr);
   a.q = q->data;
   a.q_sb = q->strides[0];
-  a.q_sh = q->strides[1];
+  a.q_sh = q->strides[hd];
+  a.n_tok = (int)n_tok;
+  a.q_st = q_st;
+  a.out_st = out_st;
+  a.lse_st = lse_st;
+  a.Hv = (int)(n_tok * Hq);
   a.lens = static_cast<const int*>(seq_lens->data);
   a.lens_s = seq_lens->strides[0];
   a.B = (int)B;
@@ -560,10 +587,10 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   a.out = out->data;
   a.out_f32 = is_f32;
   a.out_sb = out->strides[0];
-  a.out_sh = out->strides[1];
+  a.out_sh = out->strides[hd];
   a.lse = lse_out ? static_cast<float*>(lse_out->data) : nullptr;
   a.lse_sb = lse_out ? lse_out->strides[0] : 0;
-  a.lse_sh = lse_out ? lse_out->strides[1] : 0;
+  a.lse_sh = lse_out ? lse_out->strides[multi ? 2 : 1] : 0;
   a.forced_split = o.split_tokens;
   a.target_items = target_items_for(Hq, Hkv, cus);
   a.max_items = lay.max_items;

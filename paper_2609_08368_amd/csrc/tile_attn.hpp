@@ -60,15 +60,18 @@ __device__ __forceinline__ void load_q_operand(const __bf16* row, bool ok, bf16x
 }
 
 // Attention of this lane's query column over keys [t_lo, t_hi) of one KV head
-// g of the sequence whose block-table row is bt_row. Keys above `limit` are
-// masked for this column; keys below t_full are visible to every column of the
-// workgroup (no mask work for those steps). t_lo must be a multiple of kKeys.
-// Accumulates into o (O^T, 4 blocks of 32 dims), m_run (log2 units) and l_run
-// (this lane's half of the row sum; add lane ^ 32's for the total).
+// g of the sequence whose block-table row is bt_row. Keys above `limit` and
+// keys below t_min are masked for this column; keys in [t_min, t_full) are
+// visible to every column of the workgroup (no mask work for those steps).
+// t_lo must be a multiple of kKeys. A column that sees no key keeps m_run =
+// -inf and l_run = 0. Accumulates into o (O^T, 4 blocks of 32 dims), m_run
+// (log2 units) and l_run (this lane's half of the row sum; add lane ^ 32's
+// for the total).
 template <int kWaves, bool kDeep, bool kFp8 = false>
 __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, const int* bt_row, int g, int t_lo,
                                             int t_hi, int t_full, int limit, const bf16x8 (&qv)[8], TileLds& lds,
-                                            f32x16 (&o)[4], float& m_run, float& l_run, int& bad) {
+                                            f32x16 (&o)[4], float& m_run, float& l_run, int& bad,
+                                            int t_min = -1) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int col = lane & 31, kg = lane >> 5;
@@ -181,13 +184,13 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
     // folded into the exponent below); the mask only where some column cannot
     // see all of the step's keys. Keys at or beyond t_hi are masked as well.
     float mt = kNegInf;
-    if (t0 + kKeys > t_full) {
+    if (t0 + kKeys > t_full || t0 < t_min) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int key = t0 + 32 * kb + 8 * (e >> 2) + 4 * kg + (e & 3);
-          if (key > limit || key >= t_hi) sc[kb][e] = kNegInf;
+          if (key > limit || key >= t_hi || key < t_min) sc[kb][e] = kNegInf;
         }
     }
 #pragma unroll
@@ -198,18 +201,19 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
     // lazy rescale: raise the running max only when the step's max exceeds it by 2^8
     const bool raise = mt > m_run + kLazy;
     if (__builtin_amdgcn_ballot_w64(raise) != 0) {
-      const float m_new = raise ? mt : m_run;
-      const float alpha = exp2_fast(m_run - m_new);
+      // a column that does not raise keeps its state (alpha = 1, also when it
+      // has seen no key yet and m_run - m_run would be -inf + inf)
+      const float alpha = raise ? exp2_fast(m_run - mt) : 1.f;
       l_run *= alpha;
 #pragma unroll
       for (int jd = 0; jd < 4; ++jd) o[jd] *= alpha;
-      m_run = m_new;
+      m_run = raise ? mt : m_run;
     }
 
     // p = exp2(scale * log2(e) * s - m), rounded to bf16 for the PV product; the
     // row sum keeps the fp32 values (four independent partial sums)
     bf16x8 pb[4];
-    const float neg_m = -m_run;
+    const float neg_m = m_run == kNegInf ? 0.f : -m_run;    // no key seen yet: p = exp2(-inf) = 0
     float ps[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int h = 0; h < 4; ++h)
