@@ -87,16 +87,17 @@ def pmc_workload(kind: str = "ragged"):
 
     ragged: three ragged-64K decode calls, then three copies of CALIB_BYTES (the
     calibration kernel for FETCH_SIZE / WRITE_SIZE); ragged-fp8: the same with FP8
-    E4M3 pages; extend: two multi-turn extend calls; group / group-noshare: three
-    decode calls of the 16x8 trajectory-group batch with prefix sharing on / off,
-    then the same calibration copies."""
+    E4M3 pages; ragged-mtp4: the same pages with 4 query tokens per sequence;
+    extend: two multi-turn extend calls; group / group-noshare: three decode calls
+    of the 16x8 trajectory-group batch with prefix sharing on / off, then the same
+    calibration copies."""
     import torch
 
     from paper_2609_08368_amd import rl_attn as ra
     from paper_2609_08368_amd import workloads as wl
 
     dev = torch.device("cuda:0")
-    w = {"ragged": wl.decode_ragged, "ragged-fp8": wl.decode_ragged,
+    w = {"ragged": wl.decode_ragged, "ragged-fp8": wl.decode_ragged, "ragged-mtp4": wl.decode_ragged,
          "extend": wl.extend_multiturn}.get(kind, wl.decode_group_prefix)()
     fp8 = kind == "ragged-fp8"
     t = (wl.materialize_fp8 if fp8 else wl.materialize)(w, dev, poison=False)
@@ -109,6 +110,11 @@ def pmc_workload(kind: str = "ragged"):
         print(json.dumps({"pmc_workload": kind, "flops": w.flops()}), flush=True)
         return
     share = {"prefix_share": kind != "group-noshare"}
+    if kind == "ragged-mtp4":
+        g = torch.Generator(device=dev)
+        g.manual_seed(904)
+        t["q"] = torch.randn((w.batch, 4, w.hq, 128), generator=g, device=dev).to(torch.bfloat16)
+        out = torch.empty_like(t["q"])
     for _ in range(3):
         if fp8:
             ra.decode_fp8(t["q"], t["k_pages"], t["v_pages"], t["k_scale"], t["v_scale"], t["block_table"],
@@ -222,9 +228,50 @@ def summarize_pmc(fetch_dir: str, write_dir: str, fp8: bool = False):
         "algorithmic_bytes": algo,
         "traffic_over_algorithmic": (dec_fetch + dec_write) / algo,
     }
-    with open(TRAFFIC_FILE_FP8 if fp8 else TRAFFIC_FILE, "w") as f:
+    path = TRAFFIC_FILE_FP8 if fp8 else TRAFFIC_FILE
+    with open(path, "w") as f:
         json.dump(res, f, indent=1)
+    with open(path[:-5] + ".md", "w") as f:
+        f.write(traffic_markdown(res, fp8, os.path.basename(path)))
     print(json.dumps(res, indent=1))
+
+
+def traffic_markdown(d: dict, fp8: bool, json_name: str) -> str:
+    """The committed summary of one traffic measurement (written by --summarize-pmc)."""
+    kind = "ragged-fp8" if fp8 else "ragged"
+    pages = "FP8 E4M3 pages" if fp8 else "bf16 pages"
+    flag = " --fp8" if fp8 else ""
+    return f"""# HBM traffic of {d['kernel']} on the ragged 64K decode batch with {pages}
+
+Workload: B 128, Hq 96 / Hkv 8, lognormal contexts (median 16K, clipped 1K-64K), page 64;
+sum of L = 2,544,208 keys, algorithmic KV bytes {d['algorithmic_bytes']:,} per launch.
+
+Commands (repo root, one MI355X), one counter per pass:
+
+    rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch_{kind} -o run -- python bench.py --pmc-workload {kind}
+    rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write_{kind} -o run -- python bench.py --pmc-workload {kind}
+    python bench.py --summarize-pmc gpurun_out/pmc_fetch_{kind} gpurun_out/pmc_write_{kind}{flag}
+
+`--pmc-workload {kind}` runs three decode launches and then three device copies of 2 GiB
+(torch `copy_`, dispatched as `__amd_rocclr_copyBuffer`), which calibrate the counters:
+
+| counter | calibration copy (KiB / dispatch) | known bytes | scale |
+|---|---|---|---|
+| FETCH_SIZE | {d['copy_fetch_kib']:,.0f} | 2 GiB read | {d['fetch_scale']:.3f} |
+| WRITE_SIZE | {d['copy_write_kib']:,.0f} | 2 GiB written | {d['write_scale']:.3f} |
+
+| {d['kernel']} | raw KiB / dispatch | scaled bytes |
+|---|---|---|
+| FETCH_SIZE | {d['fetch_kib_per_dispatch']:,.0f} | {d['hbm_read_bytes']:,.0f} ({d['hbm_read_bytes'] / d['algorithmic_bytes']:.4f} x algorithmic) |
+| WRITE_SIZE | {d['write_kib_per_dispatch']:,.0f} | {d['hbm_write_bytes']:,.0f} (split partials) |
+| traffic | | {d['traffic_bytes']:,.0f} ({d['traffic_over_algorithmic']:.4f} x algorithmic) |
+
+Reads equal the algorithmic KV bytes: every K and V byte is fetched from HBM once, with no
+re-reads. Writes are the fp32 partials of the pieces that split a sequence (at most one per
+worker plus one per sequence). `bench.py` reports this traffic figure only while the kernel
+sources hash to the value recorded in `{json_name}` (sources under csrc/ plus build.py;
+hash {d['source_hash']}).
+"""
 
 
 def traffic_bytes(fp8: bool = False):
@@ -431,7 +478,7 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pmc-workload", nargs="?", const="ragged",
-                    choices=["ragged", "ragged-fp8", "extend", "group", "group-noshare"],
+                    choices=["ragged", "ragged-fp8", "ragged-mtp4", "extend", "group", "group-noshare"],
                     help="run only what a counter run profiles")
     ap.add_argument("--summarize-counters", metavar="PMC_DIR", help="per-kernel means of a rocprofv3 --pmc run")
     ap.add_argument("--prefix-study", action="store_true", help="time group-prefix decode with sharing on and off")
