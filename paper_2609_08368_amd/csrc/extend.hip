@@ -8,8 +8,9 @@
 // every row of a unit, so only the last steps of a unit apply the mask.
 //
 // The planner orders units longest key range first and keeps the units of one
-// (sequence, KV head) adjacent, so they run at the same time and stream the
-// same keys through the L2s.
+// (sequence, KV head) together on one XCD (workgroups go to the XCDs
+// round-robin by index), so they run at the same time and stream the same
+// keys through that XCD's L2.
 #include "kernels.hpp"
 #include "tile_attn.hpp"
 
@@ -18,6 +19,8 @@ namespace rl {
 namespace {
 
 constexpr int kSortMax = 1024;          // sequences sorted by key count up to this batch size
+constexpr int kXcds = 8;                // workgroups go to the 8 XCDs round-robin by index
+constexpr bool kXcdGroups = true;       // keep each (sequence, KV head)'s units on one XCD
 
 struct SeqRange {
   int q0, n, kv;
@@ -113,11 +116,22 @@ __global__ __launch_bounds__(1024) void plan_extend_kernel(ExtendArgs a) {
     int tot;
     const int excl = block_exclusive_scan(nt * heads, &tot, wave_tot);
     if (p < a.B) {
+      // With a multiple of 8 head groups, group gh of a sequence runs on XCD
+      // gh % 8: its units share their keys through that XCD's L2 instead of
+      // every XCD streaming every group's keys. Each XCD's units stay in list
+      // order (longest first), and every XCD gets the same number of units.
+      const bool xcd = kXcdGroups && heads % kXcds == 0;
       for (int gh = 0; gh < heads; ++gh) {
         const int g = gh / a.head_blocks, hb = gh - g * a.head_blocks;
         // last tile first: it has the longest key range of the sequence
         for (int j = 0; j < nt; ++j) {
-          const int idx = offset + excl + gh * nt + j;
+          int idx = offset + excl + gh * nt + j;
+          if (xcd) {
+            // position in the XCD's own list: units of the earlier sequences
+            // (heads / 8 groups each), then of this sequence's earlier groups
+            const int k = (offset + excl) / kXcds + (gh / kXcds) * nt + j;
+            idx = k * kXcds + gh % kXcds;
+          }
           const int i0 = (nt - 1 - j) * a.tile_tokens;
           const int cnt = min(a.tile_tokens, r.n - i0);
           if (idx < a.max_items) a.ws.items[idx] = make_int4(b, i0, cnt, g | (hb << 16));
@@ -137,10 +151,9 @@ __global__ __launch_bounds__(kExtWaves * 64, 2) void extend_mfma_kernel(ExtendAr
   __shared__ TileLds lds;
 
   // Units run in list order (longest key range first). Workgroups are handed
-  // to the XCDs round-robin, so each XCD gets every eighth unit: the work stays
-  // balanced across XCDs, and the units of one (sequence, KV head), which are
-  // adjacent in the list, run at the same time on every XCD, so each XCD's L2
-  // serves the shared keys to its share of them.
+  // to the XCDs round-robin, so each XCD takes every eighth entry; the planner
+  // lays the list out so those are the units of the (sequence, KV head) groups
+  // assigned to that XCD, which then share their keys through its L2.
   const int unit = blockIdx.x;
   if (unit >= a.ws.hdr[0]) return;
   const int4 it = a.ws.items[unit];
