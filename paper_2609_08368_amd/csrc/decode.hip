@@ -653,6 +653,8 @@ __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
 // t <= L - n_tok + i. Pieces start on 32-key tiles; the routine's steps start
 // on 64-key boundaries, so a piece's first step masks the keys before it.
 constexpr int kMultiWaves = 4;          // waves per multi-token workgroup: 128 rows
+constexpr int kXcds = 8;                // XCDs of the device; workgroup i runs on XCD i % 8
+constexpr bool kMultiXcd = true;        // a worker's workgroups on one XCD
 
 template <bool kFp8>
 __global__ __launch_bounds__(kMultiWaves * 64, 2) void decode_multi_kernel(DecodeArgs a) {
@@ -660,8 +662,20 @@ __global__ __launch_bounds__(kMultiWaves * 64, 2) void decode_multi_kernel(Decod
   const int rows = a.n_tok * a.R;
   const int nrb = (rows + kMultiWaves * kWaveRows - 1) / (kMultiWaves * kWaveRows);
   const int nch = a.Hkv * nrb;                  // workgroups per worker
-  const int worker = blockIdx.x / nch;
-  const int rem = blockIdx.x - worker * nch;
+  // Workgroups are dealt to the XCDs round-robin by index; when the workers
+  // divide evenly, worker w's workgroups (its KV heads, which read the
+  // interleaved head rows of the same tokens) are numbered so that all of
+  // them land on XCD w % 8, one after another.
+  int worker, rem;
+  if (kMultiXcd && a.max_workers % kXcds == 0) {
+    const int x = blockIdx.x % kXcds, k = blockIdx.x / kXcds;
+    const int m = k / nch;
+    rem = k - m * nch;
+    worker = x + kXcds * m;
+  } else {
+    worker = blockIdx.x / nch;
+    rem = blockIdx.x - worker * nch;
+  }
   const int g = rem % a.Hkv, rb = rem / a.Hkv;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int rr = rb * kMultiWaves * kWaveRows + wave * kWaveRows + (lane & 31);
