@@ -73,6 +73,16 @@ def test_library_exports_every_declared_symbol():
     (lambda a: a.update(q=fake([2, 8, 128], ra.RL_BF16, ptr=FAKE + 2)) or a, "RL_ERR_UNSUPPORTED", "aligned"),
     (lambda a: a.update(v=fake([10, 16, 2, 128], ra.RL_BF16, ptr=0)) or a, "RL_ERR_INVALID_ARG", "v_pages.data"),
     (lambda a: a.update(v=fake([11, 16, 2, 128], ra.RL_BF16)) or a, "RL_ERR_SHAPE", "shapes differ"),
+    # multi-token decode: q [B, n, Hq, 128] with 1 <= n <= 64, out and lse [B, n, Hq] to match
+    (lambda a: a.update(q=fake([2, 65, 8, 128], ra.RL_BF16), out=fake([2, 65, 8, 128], ra.RL_BF16)) or a,
+     "RL_ERR_UNSUPPORTED", "query tokens per sequence"),
+    (lambda a: a.update(q=fake([2, 0, 8, 128], ra.RL_BF16), out=fake([2, 0, 8, 128], ra.RL_BF16)) or a,
+     "RL_ERR_UNSUPPORTED", "query tokens per sequence"),
+    (lambda a: a.update(q=fake([2, 4, 8, 128], ra.RL_BF16)) or a, "RL_ERR_SHAPE", "out must have 4"),
+    (lambda a: a.update(q=fake([2, 4, 8, 128], ra.RL_BF16), out=fake([2, 4, 8, 128], ra.RL_BF16),
+                        lse=fake([2, 8], ra.RL_F32)) or a, "RL_ERR_SHAPE", "lse_out must have 3"),
+    (lambda a: a.update(q=fake([2, 4, 8, 128], ra.RL_BF16), out=fake([2, 4, 8, 128], ra.RL_BF16),
+                        lse=fake([2, 3, 8], ra.RL_F32)) or a, "RL_ERR_SHAPE", "lse_out shape"),
 ])
 def test_decode_validation(mutate, code, needle):
     a = mutate(decode_args())
