@@ -66,12 +66,14 @@ __device__ __forceinline__ void load_q_operand(const __bf16* row, bool ok, bf16x
 // t_lo must be a multiple of kKeys. A column that sees no key keeps m_run =
 // -inf and l_run = 0. Accumulates into o (O^T, 4 blocks of 32 dims), m_run
 // (log2 units) and l_run (this lane's half of the row sum; add lane ^ 32's
-// for the total).
+// for the total). A wave that holds no query row passes active = false: it
+// still stages its share of the rows and meets every barrier, but issues no
+// MFMA and no softmax work.
 template <int kWaves, bool kDeep, bool kFp8 = false>
 __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, const int* bt_row, int g, int t_lo,
                                             int t_hi, int t_full, int limit, const bf16x8 (&qv)[8], TileLds& lds,
                                             f32x16 (&o)[4], float& m_run, float& l_run, int& bad,
-                                            int t_min = -1) {
+                                            int t_min = -1, bool active = true) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int col = lane & 31, kg = lane >> 5;
@@ -153,88 +155,90 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
       }
     }
 
-    // S^T for the two 32-key blocks of this step; the two accumulation chains
-    // are interleaved so each MFMA's predecessor in its chain has retired
-    // K operands are read two 16-dimension slices ahead of their MFMAs; the
-    // scheduling fences keep the compiler from moving each read next to its
-    // use, which would leave one LDS read in flight per wave
-    f32x16 sc[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) sc[kb][e] = 0.f;
-    bf16x8 kop[3][2];
-    auto read_k = [&](int c, bf16x8 (&dst)[2]) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-        dst[kb] = *reinterpret_cast<const bf16x8*>(&lds.ks[buf][32 * kb + col][16 * c + 8 * kg]);
-    };
-    read_k(0, kop[0]);
-    read_k(1, kop[1]);
-#pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      if (c + 2 < 8) read_k(c + 2, kop[(c + 2) % 3]);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) sc[kb] = mfma_32x32x16(kop[c % 3][kb], qv[c], sc[kb]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-
-    // Row max of the raw scores (the positive scale commutes with max and is
-    // folded into the exponent below); the mask only where some column cannot
-    // see all of the step's keys. Keys at or beyond t_hi are masked as well.
-    float mt = kNegInf;
-    if (t0 + kKeys > t_full || t0 < t_min) {
+    if (active) {
+      // S^T for the two 32-key blocks of this step; the two accumulation chains
+      // are interleaved so each MFMA's predecessor in its chain has retired
+      // K operands are read two 16-dimension slices ahead of their MFMAs; the
+      // scheduling fences keep the compiler from moving each read next to its
+      // use, which would leave one LDS read in flight per wave
+      f32x16 sc[2];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = t0 + 32 * kb + 8 * (e >> 2) + 4 * kg + (e & 3);
-          if (key > limit || key >= t_hi || key < t_min) sc[kb][e] = kNegInf;
-        }
-    }
+        for (int e = 0; e < 16; ++e) sc[kb][e] = 0.f;
+      bf16x8 kop[3][2];
+      auto read_k = [&](int c, bf16x8 (&dst)[2]) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < 2; ++kb)
+          dst[kb] = *reinterpret_cast<const bf16x8*>(&lds.ks[buf][32 * kb + col][16 * c + 8 * kg]);
+      };
+      read_k(0, kop[0]);
+      read_k(1, kop[1]);
 #pragma unroll
-      for (int e = 0; e < 16; e += 2) mt = fmaxf(mt, fmaxf(sc[kb][e], sc[kb][e + 1]));
-    mt = max_l32(mt) * sl2;
-    // lazy rescale: raise the running max only when the step's max exceeds it by 2^8
-    const bool raise = mt > m_run + kLazy;
-    if (__builtin_amdgcn_ballot_w64(raise) != 0) {
-      // a column that does not raise keeps its state (alpha = 1, also when it
-      // has seen no key yet and m_run - m_run would be -inf + inf)
-      const float alpha = raise ? exp2_fast(m_run - mt) : 1.f;
-      l_run *= alpha;
+      for (int c = 0; c < 8; ++c) {
+        if (c + 2 < 8) read_k(c + 2, kop[(c + 2) % 3]);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int jd = 0; jd < 4; ++jd) o[jd] *= alpha;
-      m_run = raise ? mt : m_run;
-    }
-
-    // p = exp2(scale * log2(e) * s - m), rounded to bf16 for the PV product; the
-    // row sum keeps the fp32 values (four independent partial sums)
-    bf16x8 pb[4];
-    const float neg_m = m_run == kNegInf ? 0.f : -m_run;    // no key seen yet: p = exp2(-inf) = 0
-    float ps[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int h = 0; h < 4; ++h)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float p = exp2_fast(fmaf(sc[h >> 1][8 * (h & 1) + e], sl2, neg_m));
-        ps[e & 3] += p;
-        pb[h][e] = (__bf16)p;
+        for (int kb = 0; kb < 2; ++kb) sc[kb] = mfma_32x32x16(kop[c % 3][kb], qv[c], sc[kb]);
+        __builtin_amdgcn_sched_barrier(0);
       }
-    l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
 
-    // O^T += V^T P^T over the step's four 16-key groups
+      // Row max of the raw scores (the positive scale commutes with max and is
+      // folded into the exponent below); the mask only where some column cannot
+      // see all of the step's keys. Keys at or beyond t_hi are masked as well.
+      float mt = kNegInf;
+      if (t0 + kKeys > t_full || t0 < t_min) {
 #pragma unroll
-    for (int h = 0; h < 4; ++h) {
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int jd = 0; jd < 4; ++jd) {
-        const u16* vp = &lds.vs[buf][16 * h + tr_row][32 * jd + tr_col];
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)vp);
-        const i16x4 up = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vp + 8 * kVStride));
-        const i16x8 v8 = __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7);
-        o[jd] = mfma_32x32x16(__builtin_bit_cast(bf16x8, v8), pb[h], o[jd]);
+          for (int e = 0; e < 16; ++e) {
+            const int key = t0 + 32 * kb + 8 * (e >> 2) + 4 * kg + (e & 3);
+            if (key > limit || key >= t_hi || key < t_min) sc[kb][e] = kNegInf;
+          }
+      }
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; e += 2) mt = fmaxf(mt, fmaxf(sc[kb][e], sc[kb][e + 1]));
+      mt = max_l32(mt) * sl2;
+      // lazy rescale: raise the running max only when the step's max exceeds it by 2^8
+      const bool raise = mt > m_run + kLazy;
+      if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+        // a column that does not raise keeps its state (alpha = 1, also when it
+        // has seen no key yet and m_run - m_run would be -inf + inf)
+        const float alpha = raise ? exp2_fast(m_run - mt) : 1.f;
+        l_run *= alpha;
+#pragma unroll
+        for (int jd = 0; jd < 4; ++jd) o[jd] *= alpha;
+        m_run = raise ? mt : m_run;
+      }
+
+      // p = exp2(scale * log2(e) * s - m), rounded to bf16 for the PV product; the
+      // row sum keeps the fp32 values (four independent partial sums)
+      bf16x8 pb[4];
+      const float neg_m = m_run == kNegInf ? 0.f : -m_run;    // no key seen yet: p = exp2(-inf) = 0
+      float ps[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float p = exp2_fast(fmaf(sc[h >> 1][8 * (h & 1) + e], sl2, neg_m));
+          ps[e & 3] += p;
+          pb[h][e] = (__bf16)p;
+        }
+      l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
+
+      // O^T += V^T P^T over the step's four 16-key groups
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+#pragma unroll
+        for (int jd = 0; jd < 4; ++jd) {
+          const u16* vp = &lds.vs[buf][16 * h + tr_row][32 * jd + tr_col];
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)vp);
+          const i16x4 up = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vp + 8 * kVStride));
+          const i16x8 v8 = __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7);
+          o[jd] = mfma_32x32x16(__builtin_bit_cast(bf16x8, v8), pb[h], o[jd]);
+        }
       }
     }
     if (j + 1 < nsteps) {
