@@ -32,7 +32,10 @@
  * and block-table column strides below 2^24). All pointers are device pointers on the
  * current HIP device. The library only reads q, pages, tables and lengths and
  * only writes out / lse_out. Head dimension must be 128; Hq % Hkv == 0;
- * page size P must be a power of two in [8, 128].
+ * page size P must be a power of two in [8, 128]. Sizes: B <= 2^22,
+ * Hq <= 4096, B * n * Hq < 2^31 for decode (n query tokens per sequence),
+ * total_q < 2^30 for extend, num_pages and max_pages * P below 2^31
+ * (RL_ERR_UNSUPPORTED otherwise).
  *
  * Errors: every call returns RL_OK (0) or a negative RL_ERR_* code, and
  * rl_attn_last_error() returns a thread-local message for the last failure on

@@ -516,7 +516,8 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   int is_f32 = 0;
   RL_TRY(check_out(out, q, "out", &is_f32));
   RL_TRY(check_lse(lse_out, B, Hq, multi ? n_tok : 0));
-  if (B > (1 << 22) || Hq > 4096) return fail(RL_ERR_UNSUPPORTED, "batch or head count too large");
+  if (B > (1 << 22) || Hq > 4096 || B * n_tok * Hq > INT32_MAX)
+    return fail(RL_ERR_UNSUPPORTED, "batch, query tokens or head count too large");
   RL_TRY(check_data(q, "q"));
   RL_TRY(check_data(seq_lens, "seq_lens"));
   if (B == 0) return RL_OK;

@@ -83,6 +83,8 @@ def test_library_exports_every_declared_symbol():
                         lse=fake([2, 8], ra.RL_F32)) or a, "RL_ERR_SHAPE", "lse_out must have 3"),
     (lambda a: a.update(q=fake([2, 4, 8, 128], ra.RL_BF16), out=fake([2, 4, 8, 128], ra.RL_BF16),
                         lse=fake([2, 3, 8], ra.RL_F32)) or a, "RL_ERR_SHAPE", "lse_out shape"),
+    # (sequence, query row) pairs must fit 32-bit indices
+    (lambda a: a.update(**decode_args(B=1 << 22, Hq=1024, Hkv=8)) or a, "RL_ERR_UNSUPPORTED", "too large"),
 ])
 def test_decode_validation(mutate, code, needle):
     a = mutate(decode_args())
