@@ -254,6 +254,16 @@ def reserve_workspace(nbytes: int, stream=None):
     _check(lib().rl_attn_reserve_workspace(ctypes.c_size_t(nbytes), _stream(stream)))
 
 
+def decode_workspace_size(batch: int, num_q_heads: int, num_kv_heads: int, max_pages: int, page_size: int) -> int:
+    """Workspace bytes a decode call may need (n query tokens per sequence: pass n * Hq heads)."""
+    return int(lib().rl_attn_decode_workspace_size(batch, num_q_heads, num_kv_heads, max_pages, page_size))
+
+
+def extend_workspace_size(batch: int, total_q: int, num_q_heads: int, num_kv_heads: int, max_pages: int,
+                          page_size: int) -> int:
+    return int(lib().rl_attn_extend_workspace_size(batch, total_q, num_q_heads, num_kv_heads, max_pages, page_size))
+
+
 def profile_enable(on: bool = True):
     _check(lib().rl_attn_profile_enable(int(bool(on))))
 

@@ -1,0 +1,142 @@
+"""Decode and extend captured in a HIP graph (torch.cuda.CUDAGraph) after the
+workspace of the capture stream is reserved: every replay, with new query values
+copied into the captured input and eager work and synchronisations in between,
+must equal the eager call on the same inputs bit for bit (the same kernels, the
+same work split). A call that would have to grow the workspace while the stream
+is captured fails with RL_ERR_WORKSPACE instead of allocating.
+"""
+
+import pytest
+import torch
+
+from paper_2609_08368_amd import rl_attn as ra
+from paper_2609_08368_amd import workloads as wl
+from tests import gpu_helpers as H
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _replay_and_compare(g, q_static, fresh, eager, outs, what, oracle=None):
+    for rep in range(4):
+        q_new = fresh(rep)
+        q_static.copy_(q_new)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        ref = eager(q_new)                      # eager call on the default stream, in between
+        torch.cuda.synchronize()
+        for got, want in zip(outs, ref):
+            assert torch.equal(got.view(torch.int16) if got.dtype == torch.bfloat16 else got,
+                               want.view(torch.int16) if want.dtype == torch.bfloat16 else want), \
+                f"{what}: replay {rep} differs from the eager call"
+        H.say(f"  {what}: replay {rep} equal")
+    if oracle is not None:                      # the last replay against the oracle as well
+        ref_o, ref_l = oracle(q_static)
+        H.compare(outs[0].reshape(ref_o.shape), ref_o, outs[1].reshape(ref_l.shape), ref_l, what=f"{what} vs oracle")
+
+
+@pytest.mark.parametrize("fp8", [False, True])
+@pytest.mark.parametrize("n", [1, 4])
+def test_decode_graph_replays_equal_eager(fp8, n):
+    lens = [700, 4, 3000, 129, 64]
+    w = wl.custom(401, "extend" if n > 1 else "decode", lens, q_lens=[n] * len(lens) if n > 1 else None,
+                  hq=16, hkv=2, page_size=64)
+    t = (wl.materialize_fp8 if fp8 else wl.materialize)(w, DEV)
+    B, hq = w.batch, w.hq
+    shape = (B, n, hq, 128) if n > 1 else (B, hq, 128)
+    H.say(f"graph decode fp8={fp8} n={n}")
+
+    def call(q, out, lse, stream=None):
+        args = (t["k_pages"], t["v_pages"])
+        if fp8:
+            ra.decode_fp8(q, *args, t["k_scale"], t["v_scale"], t["block_table"], t["kv_lens"], t["scale"], out=out,
+                          lse=lse, stream=stream)
+        else:
+            ra.decode(q, *args, t["block_table"], t["kv_lens"], t["scale"], out=out, lse=lse, stream=stream)
+
+    def fresh(rep):
+        gen = torch.Generator(device=DEV)
+        gen.manual_seed(500 + rep)
+        return torch.randn(shape, generator=gen, device=DEV).to(torch.bfloat16)
+
+    def eager(q):
+        out = torch.empty(shape, dtype=torch.bfloat16, device=DEV)
+        lse = torch.empty(shape[:-1], dtype=torch.float32, device=DEV)
+        call(q, out, lse)
+        return out, lse
+
+    s = torch.cuda.Stream()
+    ra.reserve_workspace(ra.decode_workspace_size(B, n * hq, w.hkv, t["block_table"].shape[1], w.page_size), stream=s)
+    q_static = fresh(99)
+    out = torch.empty(shape, dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty(shape[:-1], dtype=torch.float32, device=DEV)
+    with torch.cuda.stream(s):
+        call(q_static, out, lse, stream=s)        # warm-up on the capture stream
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        call(q_static, out, lse, stream=s)
+    torch.cuda.synchronize()
+    oracle = (lambda q: H.oracle_full(w, dict(t, q=q.reshape(t["q"].shape)))) if n > 1 else \
+        (lambda q: H.oracle_full(w, dict(t, q=q)))
+    _replay_and_compare(g, q_static, fresh, eager, (out, lse), f"decode fp8={fp8} n={n}", oracle)
+    ra.check_device_errors()
+
+
+def test_extend_graph_replays_equal_eager():
+    w = wl.custom(402, "extend", [700, 300, 90], q_lens=[300, 1, 90], hq=16, hkv=2, page_size=64)
+    t = wl.materialize(w, DEV)
+    shape = tuple(t["q"].shape)
+    H.say("graph extend")
+
+    def call(q, out, lse, stream=None):
+        ra.extend(q, t["qo_indptr"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"],
+                  out=out, lse=lse, stream=stream)
+
+    def fresh(rep):
+        gen = torch.Generator(device=DEV)
+        gen.manual_seed(600 + rep)
+        return torch.randn(shape, generator=gen, device=DEV).to(torch.bfloat16)
+
+    def eager(q):
+        out = torch.empty(shape, dtype=torch.bfloat16, device=DEV)
+        lse = torch.empty(shape[:-1], dtype=torch.float32, device=DEV)
+        call(q, out, lse)
+        return out, lse
+
+    s = torch.cuda.Stream()
+    ra.reserve_workspace(ra.extend_workspace_size(w.batch, w.total_q, w.hq, w.hkv, t["block_table"].shape[1],
+                                                  w.page_size), stream=s)
+    q_static = fresh(99)
+    out = torch.empty(shape, dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty(shape[:-1], dtype=torch.float32, device=DEV)
+    with torch.cuda.stream(s):
+        call(q_static, out, lse, stream=s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        call(q_static, out, lse, stream=s)
+    torch.cuda.synchronize()
+    _replay_and_compare(g, q_static, fresh, eager, (out, lse), "extend", lambda q: H.oracle_full(w, dict(t, q=q)))
+    ra.check_device_errors()
+
+
+def test_capture_without_reserved_workspace_is_refused():
+    """A fresh stream has no workspace: the captured call reports RL_ERR_WORKSPACE and
+    launches nothing; the capture is then ended and discarded."""
+    w = wl.custom(403, "decode", [100, 40], hq=8, hkv=2, page_size=16)
+    t = wl.materialize(w, DEV)
+    s = torch.cuda.Stream()
+    out = torch.empty_like(t["q"])
+    g = torch.cuda.CUDAGraph()
+    err = None
+    with torch.cuda.graph(g, stream=s):
+        out.zero_()                             # a fill kernel, so the captured graph is not empty
+        try:
+            ra.decode(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out,
+                      stream=s)
+        except ra.RlAttnError as e:
+            err = e
+    torch.cuda.synchronize()
+    assert err is not None and err.status == "RL_ERR_WORKSPACE"
