@@ -187,10 +187,20 @@ __global__ __launch_bounds__(kExtWaves * 64, 2) void extend_mfma_kernel(ExtendAr
   const KvScales dq = kv_scales<kFp8>(a.kv, g, &bad_scale);
   const float scale = a.scale * dq.k;
   const int* bt_row = a.kv.bt + (int64_t)b * a.kv.bt_sb;
-  if (uniform_pages(a.kv))
+  // a wave whose 32 rows are all past the unit's tokens (a short chunk, or
+  // the one token of a deterministic decode) only stages
+  const bool active = __builtin_amdgcn_ballot_w64(row_ok) != 0;
+  const bool uniform = uniform_pages(a.kv);
+  if (active && uniform)
     tile_attend_pp<kExtWaves, true, kFp8>(a.kv, scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run, l_run, bad);
-  else
+  else if (active)
     tile_attend_pp<kExtWaves, false, kFp8>(a.kv, scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run, l_run, bad);
+  else if (uniform)
+    tile_attend_pp<kExtWaves, true, kFp8, false>(a.kv, scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run,
+                                                 l_run, bad);
+  else
+    tile_attend_pp<kExtWaves, false, kFp8, false>(a.kv, scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run,
+                                                  l_run, bad);
 
   const float l_tot = sum_l32(l_run);
   if (row_ok) {

@@ -282,6 +282,9 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
 // of step j-1, and every write happens after it. Both groups pass the same
 // number of barriers. The LDS buffers are still being read when the first
 // group returns: a caller that reuses them must synchronise the workgroup.
+// A wave that holds no query row runs the kCompute = false instance: it
+// stages its rows and meets every barrier but issues no MFMA and no softmax
+// work (the two instances keep the same barrier sequence).
 //
 // kUniformPages: a page holds whole steps (page size >= kKeys) and in-page
 // byte offsets fit 31 bits. A step's page id is then the same for the whole
@@ -290,7 +293,7 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
 // is formed on the scalar unit, and a thread's in-page row offsets are fixed
 // except for the clamp to the last key in the sequence's final step.
 // Otherwise every thread looks up the page of each row it stages.
-template <int kWaves, bool kUniformPages, bool kFp8 = false>
+template <int kWaves, bool kUniformPages, bool kFp8 = false, bool kCompute = true>
 __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, const int* bt_row, int g, int t_lo,
                                                int t_hi, int t_full, int limit, const bf16x8 (&qv)[8], TileLds& lds,
                                                f32x16 (&o)[4], float& m_run, float& l_run, int& bad) {
@@ -398,6 +401,7 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
   // MFMA phase: operands are read kAhead MFMAs ahead; the fences keep each
   // read ahead of the MFMAs that do not need it
   auto mfma_phase = [&](auto pv_tag, auto s_tag, int vbuf, int kbuf) {
+    if constexpr (!kCompute) return;
     constexpr bool kPV = decltype(pv_tag)::value, kS = decltype(s_tag)::value;
     constexpr int i0 = kPV ? 0 : 16, i1 = kS ? 32 : 16;
     if constexpr (kS) {
@@ -433,6 +437,7 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
 
   // softmax phase of the step starting at key t0: S^T -> P^T (bf16), running max and sum
   auto softmax_phase = [&](int t0) {
+    if constexpr (!kCompute) return;
     float mt = kNegInf;
     if (t0 + kKeys > t_full) {
 #pragma unroll
