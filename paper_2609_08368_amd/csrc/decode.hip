@@ -703,7 +703,7 @@ __global__ __launch_bounds__(kMultiWaves * 64, 2) void decode_multi_kernel(Decod
     // keys below L - n + 1 are visible to every token (t_full may not pass the
     // piece's end: the routine masks keys at or past t_hi only from t_full on)
     const int t_full = min(L - a.n_tok + 1, t_end);
-    tile_attend<kMultiWaves, false, kFp8>(a.kv, scale, a.kv.bt + (int64_t)b * a.kv.bt_sb, g, t_lo, t_end, t_full,
+    tile_attend<kMultiWaves, kFp8>(a.kv, scale, a.kv.bt + (int64_t)b * a.kv.bt_sb, g, t_lo, t_end, t_full,
                                           limit, qv, lds, o, m_run, l_run, bad, t_begin,
                                           rb * kMultiWaves * kWaveRows + wave * kWaveRows < rows);
     const HeadResult res = finish(m_run, sum_l32(l_run));
@@ -772,7 +772,7 @@ __global__ __launch_bounds__(kPrefixWaves * 64, 2) void prefix_kernel(DecodeArgs
     float m_run = kNegInf, l_run = 0.f;
     int bad = 0, bad_scale = 0;
     const KvScales dq = kv_scales<kFp8>(a.kv, g, &bad_scale);
-    tile_attend<kPrefixWaves, false, kFp8>(a.kv, a.scale * dq.k, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g, t0, t1,
+    tile_attend<kPrefixWaves, kFp8>(a.kv, a.scale * dq.k, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g, t0, t1,
                                            a.n_tok == 1 ? t1 : t0, limit, qv, lds, o, m_run, l_run, bad, -1,
                                            wave * kWaveRows / rows_m < info.y);
     const HeadResult res = finish(m_run, sum_l32(l_run));

@@ -6,7 +6,7 @@
 //
 // Per 64-key step the workgroup stages K and V of the step in LDS (double
 // buffered: the rows of a later step are fetched into registers while the
-// current step computes -- one step ahead, or two with kDeep -- and page ids
+// current step computes, one step ahead, and page ids
 // one step before the rows they address), then every wave computes
 //   S^T = K Q^T            (A = K rows from LDS, B = Q held in registers),
 //   P^T = exp2(S^T - m)    (per query column, in registers),
@@ -69,7 +69,7 @@ __device__ __forceinline__ void load_q_operand(const __bf16* row, bool ok, bf16x
 // for the total). A wave that holds no query row passes active = false: it
 // still stages its share of the rows and meets every barrier, but issues no
 // MFMA and no softmax work.
-template <int kWaves, bool kDeep, bool kFp8 = false>
+template <int kWaves, bool kFp8 = false>
 __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, const int* bt_row, int g, int t_lo,
                                             int t_hi, int t_full, int limit, const bf16x8 (&qv)[8], TileLds& lds,
                                             f32x16 (&o)[4], float& m_run, float& l_run, int& bad,
@@ -139,20 +139,12 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
   const int nsteps = (t_hi - t_lo + kKeys - 1) / kKeys;
 
   // one step: prefetch, S^T, softmax, PV, then stage the next step's rows
-  auto step = [&](int j, Rows& k_next, Rows& v_next, Rows& k_free, Rows& v_free) {
+  auto step = [&](int j, Rows& k_next, Rows& v_next) {
     const int t0 = t_lo + j * kKeys;
     const int buf = j & 1;
-    if constexpr (kDeep) {
-      // rows of step j+2 go into the set staged at the end of step j-1
-      if (j + 2 < nsteps) {
-        fetch_rows(t0 + 2 * kKeys, k_free, v_free);
-        if (j + 3 < nsteps) fetch_pages(t0 + 3 * kKeys);
-      }
-    } else {
-      if (j + 1 < nsteps) {
-        fetch_rows(t0 + kKeys, k_next, v_next);
-        if (j + 2 < nsteps) fetch_pages(t0 + 2 * kKeys);
-      }
+    if (j + 1 < nsteps) {
+      fetch_rows(t0 + kKeys, k_next, v_next);
+      if (j + 2 < nsteps) fetch_pages(t0 + 2 * kKeys);
     }
 
     if (active) {
@@ -247,26 +239,13 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
     }
   };
 
-  Rows ka, va, kb2, vb2;
+  Rows ka, va;
   fetch_pages(t_lo);
   fetch_rows(t_lo, ka, va);
   stage(0, ka, va);
   if (nsteps > 1) fetch_pages(t_lo + kKeys);
-  if constexpr (kDeep) {
-    // two steps in flight: rows of step 1 load now, page ids of step 2 too
-    if (nsteps > 1) {
-      fetch_rows(t_lo + kKeys, kb2, vb2);
-      if (nsteps > 2) fetch_pages(t_lo + 2 * kKeys);
-    }
-    __syncthreads();
-    for (int j = 0; j < nsteps; j += 2) {
-      step(j, kb2, vb2, ka, va);
-      if (j + 1 < nsteps) step(j + 1, ka, va, kb2, vb2);
-    }
-  } else {
-    __syncthreads();
-    for (int j = 0; j < nsteps; ++j) step(j, ka, va, ka, va);
-  }
+  __syncthreads();
+  for (int j = 0; j < nsteps; ++j) step(j, ka, va);
 }
 
 // The same attention with a ping-pong schedule for eight waves (two per SIMD).
