@@ -1,13 +1,14 @@
 // Multi-row attention tile on MFMA 32x32x16, shared by the extend kernel
-// (rows = chunk tokens x query heads) and the group-prefix kernel (rows =
-// trajectory-group members x query heads). A workgroup of kWaves waves owns up
-// to 32 * kWaves query rows that all read the same keys of one KV head; each
-// wave owns 32 rows, i.e. one 32-wide MFMA column block.
+// (rows = chunk tokens x query heads; tile_attend_pp), the group-prefix kernel
+// (rows = trajectory-group members x query heads) and the multi-token decode
+// kernel (rows = query tokens x query heads; both tile_attend). A workgroup of
+// kWaves waves owns up to 32 * kWaves query rows that all read the same keys
+// of one KV head; each wave owns 32 rows, i.e. one 32-wide MFMA column block.
 //
 // Per 64-key step the workgroup stages K and V of the step in LDS (double
-// buffered: the rows of a later step are fetched into registers while the
-// current step computes, one step ahead, and page ids
-// one step before the rows they address), then every wave computes
+// buffered: the rows of the next step are fetched into registers while the
+// current step computes, and page ids one step before the rows they
+// address), then every wave computes
 //   S^T = K Q^T            (A = K rows from LDS, B = Q held in registers),
 //   P^T = exp2(S^T - m)    (per query column, in registers),
 //   O^T += V^T P^T         (A = V^T read with the LDS transpose load),
