@@ -1,10 +1,11 @@
 """Shapes at the limits the library accepts, through the C-ABI, against the oracle:
 a very long single sequence (hundreds of thousands of keys, a block-table row of
 thousands of pages), a 128-wide GQA group (128 query heads on one KV head),
-the most query tokens per sequence a multi-token decode takes (64), and a
-whole prompt prefilled as one chunk.
+the most query tokens per sequence a multi-token decode takes (64), a whole
+prompt prefilled as one chunk, and batches of thousands of sequences.
 """
 
+import numpy as np
 import pytest
 
 from paper_2609_08368_amd import workloads as wl
@@ -73,3 +74,31 @@ def test_mtp_64_tokens(case):
     H.say(f"mtp n=64 case {case}")
     out, lse = run_mtp(w, t, n, split_tokens=split)
     mtp_check(w, t, n, out, lse, what=f"mtp n=64 {case}")
+
+
+def test_extend_large_batch_unsorted_plan():
+    """2,500 sequences (more than the planner sorts by key count, so units keep batch
+    order), chunks of 0-3 tokens over caches of 1-300 keys."""
+    rng = np.random.default_rng(307)
+    kv = rng.integers(1, 301, size=2500)
+    ql = np.minimum(rng.integers(0, 4, size=2500), kv)
+    w = wl.custom(307, "extend", kv.tolist(), q_lens=ql.tolist(), hq=8, hkv=2, page_size=16)
+    H.say(f"extend B=2500 total_q={w.total_q}")
+    t = wl.materialize(w, DEV)
+    out, lse = H.run_extend(w, t)
+    ref_o, ref_l = H.oracle_full(w, t)
+    H.compare(out, ref_o, lse, ref_l, what="extend B=2500")
+
+
+@pytest.mark.parametrize("deterministic", [False, True])
+def test_decode_large_batch(deterministic):
+    """3,000 sequences of 0-400 keys; the deterministic mode runs them as 3,000
+    one-row extend units through the unsorted planner path."""
+    rng = np.random.default_rng(308)
+    lens = rng.integers(0, 401, size=3000)
+    w = wl.custom(308, "decode", lens.tolist(), hq=12, hkv=1, page_size=32)
+    H.say(f"decode B=3000 deterministic={deterministic}")
+    t = wl.materialize(w, DEV)
+    out, lse = H.run_decode(w, t, deterministic=deterministic)
+    ref_o, ref_l = H.oracle_full(w, t)
+    H.compare(out, ref_o, lse, ref_l, what=f"decode B=3000 det={deterministic}")
