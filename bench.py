@@ -232,12 +232,13 @@ def summarize_pmc(fetch_dir: str, write_dir: str, fp8: bool = False):
     with open(path, "w") as f:
         json.dump(res, f, indent=1)
     with open(path[:-5] + ".md", "w") as f:
-        f.write(traffic_markdown(res, fp8, os.path.basename(path)))
+        f.write(traffic_markdown(res, fp8, os.path.basename(path), fetch_dir.rstrip("/"), write_dir.rstrip("/")))
     print(json.dumps(res, indent=1))
 
 
-def traffic_markdown(d: dict, fp8: bool, json_name: str) -> str:
-    """The committed summary of one traffic measurement (written by --summarize-pmc)."""
+def traffic_markdown(d: dict, fp8: bool, json_name: str, fetch_dir: str, write_dir: str) -> str:
+    """The committed summary of one traffic measurement (written by --summarize-pmc from the two
+    counter runs' output directories)."""
     kind = "ragged-fp8" if fp8 else "ragged"
     pages = "FP8 E4M3 pages" if fp8 else "bf16 pages"
     flag = " --fp8" if fp8 else ""
@@ -248,9 +249,9 @@ sum of L = 2,544,208 keys, algorithmic KV bytes {d['algorithmic_bytes']:,} per l
 
 Commands (repo root, one MI355X), one counter per pass:
 
-    rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch_{kind} -o run -- python bench.py --pmc-workload {kind}
-    rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write_{kind} -o run -- python bench.py --pmc-workload {kind}
-    python bench.py --summarize-pmc gpurun_out/pmc_fetch_{kind} gpurun_out/pmc_write_{kind}{flag}
+    rocprofv3 --pmc FETCH_SIZE --output-format csv -d {fetch_dir} -o run -- python bench.py --pmc-workload {kind}
+    rocprofv3 --pmc WRITE_SIZE --output-format csv -d {write_dir} -o run -- python bench.py --pmc-workload {kind}
+    python bench.py --summarize-pmc {fetch_dir} {write_dir}{flag}
 
 `--pmc-workload {kind}` runs three decode launches and then three device copies of 2 GiB
 (torch `copy_`, dispatched as `__amd_rocclr_copyBuffer`), which calibrate the counters:
@@ -499,8 +500,8 @@ def main():
         prefix_study()
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (the kernels run on one device's share; "
-              "see DESIGN.md for how the work would shard). Run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path (each GPU would serve its own "
+              "sequences or KV heads, with no exchange inside attention). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import torch
