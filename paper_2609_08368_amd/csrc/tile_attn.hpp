@@ -401,16 +401,22 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
       return *reinterpret_cast<const bf16x8*>(&lds.ks[kbuf][32 * kb + col][16 * c + 8 * kg]);
     };
     bf16x8 ring[kAhead + 1];
+    // the S^T MFMAs of this step go first, then the PV MFMAs of the previous
+    // one (independent chains; measured 2% faster with FP8 pages, the same
+    // with bf16)
+    auto at = [&](int ii) { return (kPV && kS) ? (ii < 16 ? ii + 16 : ii - 16) : i0 + ii; };
+    constexpr int n = i1 - i0;
 #pragma unroll
-    for (int i = i0; i < i0 + kAhead; ++i) ring[i % (kAhead + 1)] = read(i);
+    for (int ii = 0; ii < kAhead; ++ii) ring[ii % (kAhead + 1)] = read(at(ii));
 #pragma unroll
-    for (int i = i0; i < i1; ++i) {
-      if (i + kAhead < i1) ring[(i + kAhead) % (kAhead + 1)] = read(i + kAhead);
+    for (int ii = 0; ii < n; ++ii) {
+      const int i = at(ii);
+      if (ii + kAhead < n) ring[(ii + kAhead) % (kAhead + 1)] = read(at(ii + kAhead));
       __builtin_amdgcn_sched_barrier(0);
       if (i < 16)
-        o[i & 3] = mfma_32x32x16(ring[i % (kAhead + 1)], pb[i >> 2], o[i & 3]);
+        o[i & 3] = mfma_32x32x16(ring[ii % (kAhead + 1)], pb[i >> 2], o[i & 3]);
       else
-        sc[(i - 16) & 1] = mfma_32x32x16(ring[i % (kAhead + 1)], qv[(i - 16) >> 1], sc[(i - 16) & 1]);
+        sc[(i - 16) & 1] = mfma_32x32x16(ring[ii % (kAhead + 1)], qv[(i - 16) >> 1], sc[(i - 16) & 1]);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
