@@ -251,8 +251,8 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
 
 // The same attention with a ping-pong schedule for eight waves (two per SIMD).
 // Waves 0-3 and 4-7 form two groups that each hold one wave of every SIMD. A
-// step is split into an MFMA phase (O^T += V^T P^T of the previous step, then
-// S^T of this step) and a softmax phase, separated by workgroup barriers; the
+// step is split into an MFMA phase (S^T of this step, then O^T += V^T P^T of
+// the previous step) and a softmax phase, separated by workgroup barriers; the
 // second group starts one barrier late, so on every SIMD one wave issues MFMAs
 // while the other runs the softmax, and they swap at every barrier.
 // K is staged one step ahead of V: in its MFMA phase of step j each wave writes
