@@ -35,7 +35,9 @@ GQA expansion, scale homogeneity, batch permutation, closed-form golden file,
 FP8 E4M3 decoding against torch's float8_e4m3fn and the format's closed forms,
 FP8 pages against the same values in bf16, per-KV-head scales; KV append
 positions against a removal/append round trip, and the E4M3 encoder against
-torch's float8_e4m3fn cast, its own decoder and brute-force nearest values).
+torch's float8_e4m3fn cast, its own decoder and brute-force nearest values);
+tests/test_oracle_properties.py draws shapes, page layouts and lengths and
+compares decode and extend with dense attention computed by scipy.
 Parity with values printed in the paper is unpinned: the paper prints none.
 """
 
