@@ -2,12 +2,14 @@
 before touching the GPU (CPU only; no compute calls)."""
 
 import ctypes
+import os
 
 import pytest
 import torch
 
 from paper_2609_08368_amd import rl_attn as ra
 
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 FAKE = 0x100000          # never dereferenced: every call below fails host validation first
 
 
@@ -262,3 +264,23 @@ def test_append_validation():
     assert ra.STATUS[rc] == "RL_ERR_DTYPE"
     empty = fake([0, 2, 128], ra.RL_BF16)
     assert call(k_new=empty, v_new=empty) == "RL_OK"
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    """With no built library the binding raises instead of computing anything itself."""
+    import subprocess
+    import sys
+
+    code = ("import torch\n"
+            "from paper_2609_08368_amd import rl_attn as ra\n"
+            "try:\n"
+            "    ra.decode(torch.zeros(1, 2, 128, dtype=torch.bfloat16), torch.zeros(1, 16, 1, 128, dtype=torch.bfloat16),\n"
+            "              torch.zeros(1, 16, 1, 128, dtype=torch.bfloat16), torch.zeros(1, 1, dtype=torch.int32),\n"
+            "              torch.ones(1, dtype=torch.int32), 0.088)\n"
+            "except RuntimeError as e:\n"
+            "    print('raised:', e)\n"
+            "    raise SystemExit(0)\n"
+            "raise SystemExit(1)\n")
+    env = dict(os.environ, RL_ATTN_LIB=str(tmp_path / "absent.so"))
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0 and "is not built" in r.stdout, r.stdout + r.stderr
