@@ -146,7 +146,13 @@ __global__ __launch_bounds__(1024) void plan_extend_kernel(ExtendArgs a) {
 
 constexpr int kExtWaves = 8;            // waves per extend workgroup: 256 query rows per unit
 
-template <bool kFp8>
+// Page lookups of the tile routine, chosen on the host: one scalar id per
+// step (pages of at least 64 keys), one per wave and 32-row set (smaller
+// pages), or one per row (in-page offsets past 31 bits). Each is its own
+// kernel, so the common case keeps its register allocation.
+constexpr int kStepPages = 0, kSetPages = 1, kRowPages = 2;
+
+template <bool kFp8, int kPages>
 __global__ __launch_bounds__(kExtWaves * 64, 2) void extend_mfma_kernel(ExtendArgs a) {
   __shared__ TileLds lds;
 
@@ -190,17 +196,15 @@ __global__ __launch_bounds__(kExtWaves * 64, 2) void extend_mfma_kernel(ExtendAr
   // a wave whose 32 rows are all past the unit's tokens (a short chunk, or
   // the one token of a deterministic decode) only stages
   const bool active = __builtin_amdgcn_ballot_w64(row_ok) != 0;
-  const bool uniform = uniform_pages(a.kv);
-  if (active && uniform)
-    tile_attend_pp<kExtWaves, true, kFp8>(a.kv, scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run, l_run, bad);
-  else if (active)
-    tile_attend_pp<kExtWaves, false, kFp8>(a.kv, scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run, l_run, bad);
-  else if (uniform)
-    tile_attend_pp<kExtWaves, true, kFp8, false>(a.kv, scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run,
-                                                 l_run, bad);
+  auto attend = [&](auto compute_tag) {
+    constexpr bool kC = decltype(compute_tag)::value;
+    tile_attend_pp<kExtWaves, kPages != kRowPages, kFp8, kC, kPages == kSetPages>(
+        a.kv, scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run, l_run, bad);
+  };
+  if (active)
+    attend(std::true_type{});
   else
-    tile_attend_pp<kExtWaves, false, kFp8, false>(a.kv, scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run,
-                                                  l_run, bad);
+    attend(std::false_type{});
 
   const float l_tot = sum_l32(l_run);
   if (row_ok) {
@@ -223,10 +227,22 @@ hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream, KernelTimer* t
   plan_extend_kernel<<<1, 1024, 0, stream>>>(a);
   const unsigned grid = (unsigned)a.max_items;
   if (timer) (void)hipEventRecord(timer->start, stream);
+  const int64_t ss = a.kv.ss > a.kv.v_ss ? a.kv.ss : a.kv.v_ss;
+  const bool scalar_ids = ((int64_t)a.kv.page_size * ss + kHeadDim) * 2 < (int64_t(1) << 31);
+  const int pages = !scalar_ids ? kRowPages : (a.kv.page_size >= kKeys ? kStepPages : kSetPages);
+  auto go = [&](auto fp8_tag) {
+    constexpr bool kF = decltype(fp8_tag)::value;
+    if (pages == kStepPages)
+      extend_mfma_kernel<kF, kStepPages><<<grid, kExtWaves * 64, 0, stream>>>(a);
+    else if (pages == kSetPages)
+      extend_mfma_kernel<kF, kSetPages><<<grid, kExtWaves * 64, 0, stream>>>(a);
+    else
+      extend_mfma_kernel<kF, kRowPages><<<grid, kExtWaves * 64, 0, stream>>>(a);
+  };
   if (a.kv.k_scale)
-    extend_mfma_kernel<true><<<grid, kExtWaves * 64, 0, stream>>>(a);
+    go(std::true_type{});
   else
-    extend_mfma_kernel<false><<<grid, kExtWaves * 64, 0, stream>>>(a);
+    go(std::false_type{});
   if (timer) (void)hipEventRecord(timer->stop, stream);
   return hipGetLastError();
 }

@@ -41,11 +41,11 @@ struct TileLds {
   u16 vs[2][kKeys][kVStride];
 };
 
-// A page holds whole 64-key steps and every in-page byte offset of K and V fits
-// 31 bits (the condition of the scalar page-lookup fetch below).
+// Every in-page byte offset of K and V fits 31 bits (the condition of the
+// scalar page-lookup fetch below).
 __device__ __forceinline__ bool uniform_pages(const PagedKV& kv) {
   const int64_t ss = kv.ss > kv.v_ss ? kv.ss : kv.v_ss;
-  return kv.page_size >= kKeys && ((int64_t)kv.page_size * ss + kHeadDim) * 2 < (int64_t(1) << 31);
+  return ((int64_t)kv.page_size * ss + kHeadDim) * 2 < (int64_t(1) << 31);
 }
 
 __device__ __forceinline__ f32x16 mfma_32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
@@ -266,14 +266,17 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
 // stages its rows and meets every barrier but issues no MFMA and no softmax
 // work (the two instances keep the same barrier sequence).
 //
-// kUniformPages: a page holds whole steps (page size >= kKeys) and in-page
-// byte offsets fit 31 bits. A step's page id is then the same for the whole
-// workgroup: it is read with a scalar load (through the constant address
-// space; the block table is not written while the kernel runs), the page base
-// is formed on the scalar unit, and a thread's in-page row offsets are fixed
-// except for the clamp to the last key in the sequence's final step.
-// Otherwise every thread looks up the page of each row it stages.
-template <int kWaves, bool kUniformPages, bool kFp8 = false, bool kCompute = true>
+// kUniformPages: in-page byte offsets fit 31 bits. A wave stages four
+// consecutive key rows of each 32-row set of a step, and pages hold at least
+// eight keys, so each set's page id is the same for the whole wave (kSetPages,
+// for pages of fewer than 64 keys; otherwise one id serves the whole step and
+// workgroup): it is read with a scalar load
+// (through the constant address space; the block table is not written while
+// the kernel runs), the page base is formed on the scalar unit, and a thread's
+// in-page row offsets are fixed except for the clamp to the last key in the
+// sequence's final step, which stays in the page of its set. Otherwise every
+// thread looks up the page of each row it stages.
+template <int kWaves, bool kUniformPages, bool kFp8 = false, bool kCompute = true, bool kSetPages = false>
 __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, const int* bt_row, int g, int t_lo,
                                                int t_hi, int t_full, int limit, const bf16x8 (&qv)[8], TileLds& lds,
                                                f32x16 (&o)[4], float& m_run, float& l_run, int& bad) {
@@ -343,34 +346,51 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
   const ConstInt* bt_c = (const ConstInt*)bt_row;
   const char* kbase_u = (const char*)kv.k + ES * ((int64_t)g * kv.sh);
   const char* vbase_u = (const char*)kv.v + ES * ((int64_t)g * kv.v_sh);
-  uint32_t koff[kStageRows], voff[kStageRows];        // byte offsets of this thread's rows in a step
+  // byte offsets of this thread's rows in their pages (for a page of at least
+  // a step, relative to the step's first key)
+  uint32_t koff[kStageRows], voff[kStageRows];
 #pragma unroll
   for (int i = 0; i < kStageRows; ++i) {
-    koff[i] = ES * (ld_chunk + (uint32_t)(ld_row + kRowStep * i) * kss);
-    voff[i] = ES * (ld_chunk + (uint32_t)(ld_row + kRowStep * i) * vss);
+    koff[i] = ES * (ld_chunk + ((uint32_t)(ld_row + kRowStep * i) & (uint32_t)pmask) * kss);
+    voff[i] = ES * (ld_chunk + ((uint32_t)(ld_row + kRowStep * i) & (uint32_t)pmask) * vss);
   }
-  auto page_id = [&](int t0) -> int {
-    const int t = t0 < t_last ? t0 : t_last;
-    int pg = bt_c[__umul24((uint32_t)(t >> kv.log2_page), bt_sj)];
-    if ((unsigned)pg >= (unsigned)kv.num_pages) {
-      bad = 1;
-      pg = pg < 0 ? 0 : kv.num_pages - 1;
-    }
-    return pg;
-  };
-  auto fetch_u = [&](int t0, int pg, const char* base, int64_t sp, uint32_t ss, const uint32_t (&off)[kStageRows],
-                     Rows& r) {
+  const int wave_row = __builtin_amdgcn_readfirstlane(4 * (tid >> 6));   // the wave's first row of a set
+  typedef int Pids[kStageRows];
+  // page ids of the wave's row sets of the step starting at t0 (one page for
+  // the whole step unless kSetPages)
+  auto page_ids = [&](int t0, Pids& p) {
     const int tc = t0 < t_last ? t0 : t_last;
-    const char* pb = base + ES * ((int64_t)pg * sp) + ES * ((uint32_t)(tc & pmask) * ss);
+#pragma unroll
+    for (int i = 0; i < kStageRows; ++i) {
+      if (!kSetPages && i > 0) {
+        p[i] = p[0];
+        continue;
+      }
+      int t = kSetPages ? tc + wave_row + kRowStep * i : tc;
+      t = t < t_hi ? t : t_hi - 1;
+      int pg = bt_c[__umul24((uint32_t)(t >> kv.log2_page), bt_sj)];
+      if ((unsigned)pg >= (unsigned)kv.num_pages) {
+        bad = 1;
+        pg = pg < 0 ? 0 : kv.num_pages - 1;
+      }
+      p[i] = pg;
+    }
+  };
+  auto fetch_u = [&](int t0, const Pids& p, const char* base, int64_t sp, uint32_t ss,
+                     const uint32_t (&off)[kStageRows], Rows& r) {
+    const int tc = t0 < t_last ? t0 : t_last;
+    const uint32_t step_off = ES * ((uint32_t)(tc & pmask) * ss);   // zero when a page holds at most a step
     if (tc + kKeys <= t_hi) {
 #pragma unroll
-      for (int i = 0; i < kStageRows; ++i) r[i] = load_kv_raw<kFp8>(pb + off[i]);
+      for (int i = 0; i < kStageRows; ++i)
+        r[i] = load_kv_raw<kFp8>(base + ES * ((int64_t)p[i] * sp) + step_off + off[i]);
     } else {
       const int last = t_hi - 1 - tc;
 #pragma unroll
       for (int i = 0; i < kStageRows; ++i) {
         const int rr = min(ld_row + kRowStep * i, last);
-        r[i] = load_kv_raw<kFp8>(pb + ES * (ld_chunk + (uint32_t)rr * ss));
+        r[i] = load_kv_raw<kFp8>(base + ES * ((int64_t)p[i] * sp) +
+                                 ES * (ld_chunk + ((uint32_t)(tc + rr) & (uint32_t)pmask) * ss));
       }
     }
   };
@@ -467,15 +487,16 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
   // ids (or scalar page ids) of steps j+1 and j+2 are at hand.
   Rows kr, vr;
   Ids id_k, id_v;
-  int pid_1 = 0, pid_2 = 0;
+  Pids pid_1 = {}, pid_2 = {};
   if constexpr (kUniformPages) {
-    const int p0 = page_id(t_lo);
+    Pids p0;
+    page_ids(t_lo, p0);
     fetch_u(t_lo, p0, kbase_u, kv.sp, kss, koff, kr);
     fetch_u(t_lo, p0, vbase_u, kv.v_sp, vss, voff, vr);
     put_k(0, kr);
-    pid_1 = page_id(t_lo + kKeys);
+    page_ids(t_lo + kKeys, pid_1);
     fetch_u(t_lo + kKeys, pid_1, kbase_u, kv.sp, kss, koff, kr);
-    pid_2 = page_id(t_lo + 2 * kKeys);
+    page_ids(t_lo + 2 * kKeys, pid_2);
   } else {
     load_ids(t_lo, id_k);
     fetch(t_lo, id_k, kbase, ksp, kss, kr);
@@ -495,7 +516,8 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
     if constexpr (kUniformPages) {
       fetch_u(t0 + kKeys, pid_1, vbase_u, kv.v_sp, vss, voff, vr);
       fetch_u(t0 + 2 * kKeys, pid_2, kbase_u, kv.sp, kss, koff, kr);
-      pid_1 = pid_2;
+#pragma unroll
+      for (int i = 0; i < kStageRows; ++i) pid_1[i] = pid_2[i];
     } else {
       fetch(t0 + kKeys, id_v, vbase, vsp, vss, vr);
       fetch(t0 + 2 * kKeys, id_k, kbase, ksp, kss, kr);
@@ -507,7 +529,7 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
   // the scalar page id of step j+3 is read at the end of step j's softmax
   // phase, so the barrier's wait covers its latency
   auto next_page = [&](int j) {
-    if constexpr (kUniformPages) pid_2 = page_id(t_lo + (j + 3) * kKeys);
+    if constexpr (kUniformPages) page_ids(t_lo + (j + 3) * kKeys, pid_2);
   };
   const std::true_type yes{};
   const std::false_type no{};
