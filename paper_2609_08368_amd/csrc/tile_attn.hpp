@@ -41,13 +41,6 @@ struct TileLds {
   u16 vs[2][kKeys][kVStride];
 };
 
-// Every in-page byte offset of K and V fits 31 bits (the condition of the
-// scalar page-lookup fetch below).
-__device__ __forceinline__ bool uniform_pages(const PagedKV& kv) {
-  const int64_t ss = kv.ss > kv.v_ss ? kv.ss : kv.v_ss;
-  return ((int64_t)kv.page_size * ss + kHeadDim) * 2 < (int64_t(1) << 31);
-}
-
 __device__ __forceinline__ f32x16 mfma_32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
