@@ -116,9 +116,15 @@ _DTYPES = {torch.bfloat16: RL_BF16, torch.float32: RL_F32, torch.int32: RL_I32,
 
 
 def view(t: Optional[torch.Tensor]):
-    """An ``rl_tensor`` describing ``t`` (no copy); None -> NULL."""
+    """An ``rl_tensor`` describing ``t`` (no copy); None -> NULL.
+
+    The library dereferences the pointers on the current HIP device, so every
+    tensor must live there (a host pointer would reach a kernel)."""
     if t is None:
         return None
+    if not t.is_cuda or t.device.index != torch.cuda.current_device():
+        raise ValueError(f"tensor on {t.device}: the library reads and writes tensors on the current device "
+                         f"(cuda:{torch.cuda.current_device() if torch.cuda.is_available() else '?'})")
     if t.dim() > 4:
         raise ValueError("rl_tensor holds at most 4 dimensions")
     v = RlTensor()

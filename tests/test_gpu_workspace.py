@@ -74,3 +74,19 @@ def test_failed_allocation_is_reported():
     H.say("subprocess with forced allocation failure")
     r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True, text=True, timeout=200)
     assert r.returncode == 0 and "status RL_ERR_WORKSPACE" in r.stdout, r.stdout + r.stderr
+
+
+def test_host_tensor_is_refused():
+    """A tensor that is not on the current device never reaches the library: the
+    binding raises before any call (a host pointer would reach a kernel)."""
+    w = wl.custom(505, "decode", [100, 40], hq=8, hkv=2, page_size=16)
+    t = wl.materialize(w, DEV)
+    for name in ("q", "k_pages", "block_table", "kv_lens"):
+        args = dict(t)
+        args[name] = t[name].cpu()
+        with pytest.raises(ValueError, match="current device"):
+            ra.decode(args["q"], args["k_pages"], args["v_pages"], args["block_table"], args["kv_lens"], t["scale"])
+    out_host = torch.empty(t["q"].shape, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="current device"):
+        ra.decode(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out_host)
+    ra.check_device_errors()
