@@ -232,10 +232,14 @@ Profiler& prof() {
 }
 
 // Returns a timer to pass to a launch when profiling is on (else nullptr).
-rl::KernelTimer* prof_timer(rl::KernelTimer* slot) {
+rl::KernelTimer* prof_timer(rl::KernelTimer* slot, hipStream_t st) {
   Profiler& p = prof();
   std::lock_guard<std::mutex> lk(p.mu);
   if (!p.on) return nullptr;
+  // a call being captured into a graph is not timed (its events would only
+  // be recorded at replay)
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return nullptr;
   if (hipEventCreate(&slot->start) != hipSuccess) return nullptr;
   if (hipEventCreate(&slot->stop) != hipSuccess) {
     (void)hipEventDestroy(slot->start);
@@ -480,7 +484,7 @@ int run_extend(rl::ExtendArgs& a, hipStream_t st, int prof_kind) {
   a.ws.items = reinterpret_cast<int4*>(base + 256);
   a.ws.err = w->err;
   rl::KernelTimer slot;
-  rl::KernelTimer* timer = prof_timer(&slot);
+  rl::KernelTimer* timer = prof_timer(&slot, st);
   hipError_t e = rl::launch_extend(a, st, timer);
   prof_commit(prof_kind, timer);
   if (e != hipSuccess) return hip_fail(e, "extend kernel launch");
@@ -612,7 +616,7 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   a.ws.part_lse = reinterpret_cast<float*>(base + lay.off_pl);
   a.ws.err = w->err;
   rl::KernelTimer slot;
-  rl::KernelTimer* timer = prof_timer(&slot);
+  rl::KernelTimer* timer = prof_timer(&slot, st);
   e = rl::launch_decode(a, st, timer);
   prof_commit(0, timer);
   if (e != hipSuccess) return hip_fail(e, "decode kernel launch");
@@ -749,7 +753,7 @@ int append_impl(const rl_tensor* k_new, const rl_tensor* v_new, const rl_tensor*
   a.max_pages = kv.max_pages;
   a.err = w->err;
   rl::KernelTimer slot;
-  rl::KernelTimer* timer = prof_timer(&slot);
+  rl::KernelTimer* timer = prof_timer(&slot, st);
   hipError_t e = rl::launch_append(a, st, timer);
   prof_commit(2, timer);
   if (e != hipSuccess) return hip_fail(e, "append kernel launch");

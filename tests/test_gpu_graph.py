@@ -140,3 +140,30 @@ def test_capture_without_reserved_workspace_is_refused():
             err = e
     torch.cuda.synchronize()
     assert err is not None and err.status == "RL_ERR_WORKSPACE"
+
+
+def test_profiling_skips_captured_calls():
+    """With kernel timing on, a call captured into a graph is not timed (its events
+    would only be recorded at replay); eager calls still are."""
+    w = wl.custom(404, "decode", [300, 64], hq=8, hkv=2, page_size=16)
+    t = wl.materialize(w, DEV)
+    s = torch.cuda.Stream()
+    ra.reserve_workspace(ra.decode_workspace_size(w.batch, w.hq, w.hkv, t["block_table"].shape[1], w.page_size),
+                         stream=s)
+    out = torch.empty_like(t["q"])
+    ra.profile_read("decode")
+    ra.profile_enable(True)
+    try:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            ra.decode(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out,
+                      stream=s)
+        g.replay()
+        ra.decode(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"])
+        torch.cuda.synchronize()
+        launches, ms = ra.profile_read("decode")
+    finally:
+        ra.profile_enable(False)
+    assert launches == 1 and ms > 0, (launches, ms)
+    ref_o, _ = H.oracle_full(w, t)
+    H.compare(out, ref_o, what="captured decode with profiling on")
