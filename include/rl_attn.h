@@ -50,6 +50,12 @@
  * Memory: the library owns one workspace per (device, stream), grown with
  * hipMalloc on demand (or ahead of time with rl_attn_reserve_workspace) and
  * never grown while the stream is being captured (RL_ERR_WORKSPACE instead).
+ * A graph captured on a stream uses that stream's workspace when replayed:
+ * replay it on the capture stream (or ordered with it), since calls that share
+ * a workspace must not overlap. Once a call was captured on a stream, a later
+ * growth of its workspace keeps the old buffer allocated, so graphs captured
+ * before stay valid; rl_attn_release() frees it, after which such graphs must
+ * not be replayed.
  */
 #ifndef RL_ATTN_H
 #define RL_ATTN_H
@@ -256,7 +262,9 @@ size_t rl_attn_extend_workspace_size(int64_t batch, int64_t total_q, int64_t num
 int rl_attn_profile_enable(int on);
 int rl_attn_profile_read(int kind, int* launches, double* mean_ms);
 
-/* Frees every workspace the library holds (synchronises the device first). */
+/* Frees every workspace the library holds (synchronises the device first),
+ * including buffers kept for graphs captured earlier: replaying such a graph
+ * afterwards is an error. */
 void rl_attn_release(void);
 
 #ifdef __cplusplus

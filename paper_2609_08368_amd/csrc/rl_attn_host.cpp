@@ -158,6 +158,11 @@ struct Workspace {
   void* ptr = nullptr;
   size_t size = 0;
   int* err = nullptr;
+  // set once a call on this stream was captured into a graph: the graph keeps
+  // the buffer's address, so a later growth retires the buffer (freed by
+  // rl_attn_release) instead of freeing it
+  bool captured = false;
+  std::vector<void*> retired;
 };
 
 std::mutex g_mu;
@@ -184,9 +189,12 @@ int acquire_ws(hipStream_t st, size_t need, Workspace** out) {
   Workspace& w = g_ws[{dev, st}];
   const bool need_err = w.err == nullptr;
   const bool grow = w.size < need;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  e = hipStreamIsCapturing(st, &cs);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamIsCapturing");
+  const bool capturing = cs != hipStreamCaptureStatusNone;
   if (need_err || grow) {
-    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-    if (hipStreamIsCapturing(st, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone)
+    if (capturing)
       return fail(RL_ERR_WORKSPACE,
                   "workspace must grow to %zu bytes while the stream is being captured; call "
                   "rl_attn_reserve_workspace first",
@@ -205,7 +213,10 @@ int acquire_ws(hipStream_t st, size_t need, Workspace** out) {
     if (w.ptr) {
       e = hipStreamSynchronize(st);
       if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
-      (void)hipFree(w.ptr);
+      if (w.captured)
+        w.retired.push_back(w.ptr);
+      else
+        (void)hipFree(w.ptr);
       w.ptr = nullptr;
       w.size = 0;
     }
@@ -215,6 +226,7 @@ int acquire_ws(hipStream_t st, size_t need, Workspace** out) {
     w.ptr = p;
     w.size = need;
   }
+  if (capturing) w.captured = true;
   *out = &w;
   return RL_OK;
 }
@@ -1050,6 +1062,7 @@ void rl_attn_release(void) {
   (void)hipDeviceSynchronize();
   for (auto& kv : g_ws) {
     if (kv.second.ptr) (void)hipFree(kv.second.ptr);
+    for (void* r : kv.second.retired) (void)hipFree(r);
     if (kv.second.err) (void)hipFree(kv.second.err);
   }
   g_ws.clear();

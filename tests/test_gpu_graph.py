@@ -167,3 +167,43 @@ def test_profiling_skips_captured_calls():
     assert launches == 1 and ms > 0, (launches, ms)
     ref_o, _ = H.oracle_full(w, t)
     H.compare(out, ref_o, what="captured decode with profiling on")
+
+
+def test_graph_survives_workspace_growth():
+    """A graph keeps the address of its stream's workspace: a later, larger eager call
+    on the same stream grows the workspace but keeps the captured buffer, so the graph
+    still replays correctly; rl_attn_release() then frees both."""
+    w = wl.custom(405, "decode", [300, 64], hq=8, hkv=2, page_size=16)
+    t = wl.materialize(w, DEV)
+    big = wl.custom(406, "decode", [40] * 4000, hq=8, hkv=2, page_size=16)
+    tb = wl.materialize(big, DEV)
+    s = torch.cuda.Stream()
+    ra.reserve_workspace(ra.decode_workspace_size(w.batch, w.hq, w.hkv, t["block_table"].shape[1], w.page_size),
+                         stream=s)
+    out = torch.empty_like(t["q"])
+    lse = torch.empty(t["q"].shape[:-1], dtype=torch.float32, device=DEV)
+    H.say("graph then workspace growth on the capture stream")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        ra.decode(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out, lse=lse,
+                  stream=s)
+    torch.cuda.synchronize()
+    out_big = torch.empty_like(tb["q"])
+    with torch.cuda.stream(s):
+        ra.decode(tb["q"], tb["k_pages"], tb["v_pages"], tb["block_table"], tb["kv_lens"], tb["scale"], out=out_big,
+                  stream=s)                     # needs a larger workspace: it grows here
+    torch.cuda.synchronize()
+    want_o, want_l = H.run_decode(w, t)
+    for rep in range(3):
+        out.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), want_o.view(torch.int16)) and torch.equal(lse, want_l), \
+            f"replay {rep} after the workspace grew differs from the eager call"
+    ref_o, ref_l = H.oracle_full(w, t)
+    H.compare(out, ref_o, lse, ref_l, what="graph replay after workspace growth")
+    ref_bo, ref_bl = H.oracle_full(big, tb)
+    H.compare(out_big, ref_bo, what="larger call on the capture stream")
+    ra.check_device_errors(s)
+    del g
+    ra.release()
