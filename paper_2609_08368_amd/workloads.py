@@ -210,7 +210,7 @@ def custom(seed: int, kind: str, kv_lens, q_lens=None, hq: int = 8, hkv: int = 2
                  kv_head_scale=scales, shared_prefix_pages=shared_tokens // page_size, group_size=group_size)
 
 
-CONFIGS = {
+WORKLOADS = {
     "decode_tiny": decode_tiny,
     "decode_uniform": decode_uniform,
     "decode_ragged": decode_ragged,

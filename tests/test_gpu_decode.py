@@ -119,7 +119,7 @@ def test_decode_strided_views():
 @pytest.mark.parametrize("name", ["decode_uniform", "decode_ragged", "decode_group_prefix", "decode_group_long_prefix"])
 def test_decode_full_size_sampled(name):
     """Full-size workloads in the benchmark's launch configuration; sampled sequences vs the oracle."""
-    w = wl.CONFIGS[name]() if name in wl.CONFIGS else getattr(wl, name)()
+    w = wl.WORKLOADS[name]() if name in wl.WORKLOADS else getattr(wl, name)()
     H.say(f"full size {name}: B={w.batch} sum(L)={int(w.kv_lens.sum())}")
     t = wl.materialize(w, DEV)
     out, lse = H.run_decode(w, t)
