@@ -7,7 +7,7 @@ from paper_2609_08368_amd import workloads as wl
 
 
 def test_metadata_deterministic():
-    for name, fn in wl.CONFIGS.items():
+    for name, fn in wl.WORKLOADS.items():
         a, b = fn(), fn()
         assert np.array_equal(a.block_table, b.block_table), name
         assert np.array_equal(a.kv_lens, b.kv_lens), name
