@@ -70,6 +70,7 @@ EXTEND_CASES = [
     (128, 8, 1, [600], [257]),
     (32, 16, 16, [200, 50], [150, 7]),               # one query head per KV head
     (16, 8, 2, [30, 0, 12], [0, 0, 12]),             # empty chunks
+    (8, 12, 3, [90, 13, 200], [20, 13, 70]),         # pages of 8 keys: eight pages per 64-key step
 ]
 
 
