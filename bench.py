@@ -6,8 +6,11 @@ One step = one pass of the whole path over resident synthetic batches:
   * decode with trajectory-group prefix sharing (16 prompts x G=8, shared
     4096-token prefix, private continuations U{512..16384});
   * extend (B=32, cached prefix U{8K..64K}, appended chunk U{64..2048}).
-Prints one JSON line. ``value`` is the decode KV-bytes rate of the ragged 64K
-batch; the extend and prefix-group figures are reported beside it.
+The tiny (B=4) and uniform (B=64 x 8192 keys) decode batches are timed beside
+the step. Prints one JSON line. ``value`` is the decode KV-bytes rate of the
+ragged 64K batch; every other workload's figures (mean, median, min and p90
+call times, rates, roofline fractions) and the float64 oracle's rate on the
+host cores for each workload are reported beside it.
 """
 
 from __future__ import annotations
@@ -22,6 +25,23 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+
+def _host_threads() -> int:
+    """Host threads of the oracle baseline: the affinity set, capped by an
+    OMP_NUM_THREADS the environment already sets."""
+    n = len(os.sched_getaffinity(0))
+    try:
+        n = min(n, int(os.environ.get("OMP_NUM_THREADS", n)))
+    except ValueError:
+        pass
+    return max(1, n)
+
+
+# BLAS thread counts are pinned before numpy is first imported
+HOST_THREADS = _host_threads()
+for _v in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS"):
+    os.environ[_v] = str(HOST_THREADS)
+
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 MFMA_BF16_PEAK_TFLOPS = 2516.6  # MI355X dense bf16 MFMA (256 CU x 4096 flop/clk x 2.4 GHz)
 METRIC = "decode-attention KV GB/s (% of HBM peak) + extend TFLOP/s at 64k ctx"
@@ -31,36 +51,90 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(w, tensors, budget_s: float):
-    """The float64 oracle on a bounded sample of the decode batch (host cores)."""
+def cpu_oracle(w, tensors, budget_s: float, threads: int = HOST_THREADS) -> dict:
+    """The float64 oracle, as it stands, on a bounded sample of one workload, on the host cores.
+
+    Decode: one sequence (all its heads) at a time in batch order, BLAS on
+    ``threads`` threads (the oracle's page gather is a Python loop, so a thread
+    pool would only contend for the interpreter). Extend: independent (sequence,
+    KV head) pairs in a seeded random order on a pool of ``threads`` threads with
+    one BLAS thread each (large matrix products and ufuncs, which release the
+    interpreter), in rounds of ``threads`` pairs. Either runs until ``budget_s``
+    of wall time has passed (or all are done). Returns the rate over the tasks
+    done, scaled to the metric's units."""
+    import concurrent.futures
+
     import numpy as np
+    import torch
+    from threadpoolctl import threadpool_limits
 
     import oracle
     from paper_2609_08368_amd import workloads as wl
 
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
-    except Exception:  # threadpoolctl missing: report the affinity set
-        threads = len(os.sched_getaffinity(0))
-    # smallest-first sample of sequences, grown until the estimated time budget is used
-    order = np.argsort(w.kv_lens, kind="stable")
-    done_tokens, elapsed, rows_done = 0, 0.0, 0
-    for b in order:
-        sub = wl.compact_subset(w, tensors, [int(b)])
-        t0 = time.perf_counter()
-        oracle.decode(sub["q"], sub["k_pages"], sub["v_pages"], sub["block_table"], sub["kv_lens"], tensors["scale"])
-        elapsed += time.perf_counter() - t0
-        done_tokens += int(w.kv_lens[b])
-        rows_done += 1
-        if elapsed >= budget_s:
-            break
-    kv_bytes = done_tokens * w.hkv * 128 * 2 * 2
-    which = (f"all {rows_done} sequences" if rows_done == len(order)
-             else f"the {rows_done} shortest of {len(order)} sequences")
-    return {"value": round(kv_bytes / elapsed / 1e9, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"float64 oracle decode of {which} of the ragged 64K batch "
-                      f"({done_tokens} keys, {kv_bytes / 1e9:.2f} GB of KV) in {elapsed:.1f} s"}
+    def bits(t):
+        return wl.to_numpy_bits(t) if t.dtype == torch.bfloat16 else t.cpu().numpy()
+
+    q, kp, vp = bits(tensors["q"]), bits(tensors["k_pages"]), bits(tensors["v_pages"])
+    bt, lens, scale = w.block_table, w.kv_lens, tensors["scale"]
+    hkv, hq = w.hkv, w.hq
+    r = hq // hkv
+    if w.kind == "decode":
+        tasks = [(b,) for b in range(w.batch)]
+    else:
+        indptr = w.qo_indptr
+        tasks = [(b, g) for b in range(w.batch) for g in range(hkv) if w.q_lens[b] > 0]
+        tasks = [tasks[i] for i in np.random.default_rng(w.seed).permutation(len(tasks))]
+
+    def run(task):
+        if w.kind == "decode":
+            (b,) = task
+            oracle.decode(q[b:b + 1], kp, vp, bt[b:b + 1], lens[b:b + 1], scale)
+            return int(lens[b]) * hkv * 512, 1.0, 4.0 * hq * 128 * int(lens[b])
+        b, g = task
+        q0, q1 = int(indptr[b]), int(indptr[b + 1])
+        n, p = q1 - q0, int(lens[b]) - (q1 - q0)
+        oracle.extend(q[q0:q1, g * r:(g + 1) * r], np.array([0, n], np.int32), kp[:, :, g:g + 1], vp[:, :, g:g + 1],
+                      bt[b:b + 1], lens[b:b + 1], scale)
+        return (n + p) * 512, n / hkv, 4.0 * r * 128 * (n * p + n * (n + 1) / 2)
+
+    done = 0
+    kv_bytes = tokens = flops = 0.0
+    t0 = time.perf_counter()
+    if w.kind == "decode":
+        with threadpool_limits(threads, "blas"):
+            while done < len(tasks) and time.perf_counter() - t0 < budget_s:
+                kb, tk, fl = run(tasks[done])
+                kv_bytes, tokens, flops, done = kv_bytes + kb, tokens + tk, flops + fl, done + 1
+        how = f"one sequence at a time, BLAS on {threads} threads"
+    else:
+        with threadpool_limits(1, "blas"), concurrent.futures.ThreadPoolExecutor(threads) as ex:
+            while done < len(tasks) and time.perf_counter() - t0 < budget_s:
+                for kb, tk, fl in ex.map(run, tasks[done:done + threads]):
+                    kv_bytes += kb
+                    tokens += tk
+                    flops += fl
+                done = min(len(tasks), done + threads)
+        how = f"{threads} threads, one BLAS thread each"
+    wall = time.perf_counter() - t0
+    unit_what = "sequences" if w.kind == "decode" else "(sequence, KV head) pairs"
+    res = {"cores": int(threads), "kind": "oracle", "wall_s": round(wall, 3), "tasks": done, "of": len(tasks),
+           "tokens_per_s": round(tokens / wall, 2),
+           "sample": f"float64 oracle over {done} of {len(tasks)} {unit_what} of {w.name} "
+                     f"({kv_bytes / 1e9:.3f} GB of KV, {flops / 1e12:.3f} TFLOP) in {wall:.2f} s ({how})"}
+    if w.kind == "decode":
+        res.update({"value": round(kv_bytes / wall / 1e9, 4), "unit": "GB/s"})
+    else:
+        res.update({"value": round(flops / wall / 1e12, 6), "unit": "TFLOP/s"})
+    return res
+
+
+def timing_stats(v) -> dict:
+    """Mean, median, min and 90th percentile of per-call times (ms)."""
+    v = sorted(v)
+    n = len(v)
+    p90 = v[min(n - 1, int(math.ceil(0.9 * n)) - 1)]
+    return {"ms_mean": round(sum(v) / n, 4), "ms_median": round(v[n // 2] if n % 2 else 0.5 * (v[n // 2 - 1] + v[n // 2]), 4),
+            "ms_min": round(v[0], 4), "ms_p90": round(p90, 4), "calls": n}
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_ragged64k_hbm_traffic.json")
@@ -476,7 +550,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="scales the oracle baseline's wall-time budgets (15: 33 s over the five workloads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pmc-workload", nargs="?", const="ragged",
                     choices=["ragged", "ragged-fp8", "ragged-mtp4", "extend", "group", "group-noshare"],
@@ -513,28 +588,32 @@ def main():
     torch.cuda.set_device(dev)
     ra.lib()
     log("materialising inputs on the GPU ...")
+    w_tiny = wl.decode_tiny()
+    w_uni = wl.decode_uniform()
     w_dec = wl.decode_ragged()
     w_grp = wl.decode_group_prefix()
     w_ext = wl.extend_multiturn()
+    t_tiny = wl.materialize(w_tiny, dev, poison=False)
+    t_uni = wl.materialize(w_uni, dev, poison=False)
     t_dec = wl.materialize(w_dec, dev, poison=False)
     t_grp = wl.materialize(w_grp, dev, poison=False)
     t_ext = wl.materialize(w_ext, dev, poison=False)
-    out_dec = torch.empty_like(t_dec["q"])
-    out_grp = torch.empty_like(t_grp["q"])
-    out_ext = torch.empty_like(t_ext["q"])
+    outs = {id(t): torch.empty_like(t["q"]) for t in (t_tiny, t_uni, t_dec, t_grp, t_ext)}
     torch.cuda.synchronize()
     log(f"ragged decode: sum(L)={int(w_dec.kv_lens.sum())}  group decode: sum(L)={int(w_grp.kv_lens.sum())}  "
         f"extend: total_q={w_ext.total_q}")
 
-    def decode(w, t, out):
-        ra.decode_plain(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out)
+    def decode(t):
+        ra.decode_plain(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"],
+                        out=outs[id(t)])
 
     def extend():
         ra.extend_plain(t_ext["q"], t_ext["qo_indptr"], t_ext["k_pages"], t_ext["v_pages"], t_ext["block_table"],
-                        t_ext["kv_lens"], t_ext["scale"], out=out_ext)
+                        t_ext["kv_lens"], t_ext["scale"], out=outs[id(t_ext)])
 
-    parts = [("decode_ragged", lambda: decode(w_dec, t_dec, out_dec)),
-             ("decode_group_prefix", lambda: decode(w_grp, t_grp, out_grp)),
+    # one step: the headline decode, the trajectory-group decode and the extend
+    parts = [("decode_ragged", lambda: decode(t_dec)),
+             ("decode_group_prefix", lambda: decode(t_grp)),
              ("extend_multiturn", extend)]
     for _ in range(args.warmup):
         for _, fn in parts:
@@ -564,9 +643,7 @@ def main():
     n_dec, dec_kernel_ms_all = ra.profile_read("decode")
     n_ext, ext_kernel_ms = ra.profile_read("extend")
     total_ms = step_start.elapsed_time(step_stop)
-    ms = {name: sorted(a.elapsed_time(b) for a, b in ev[name]) for name in ev}
-    med = {name: v[len(v) // 2] for name, v in ms.items()}
-    mean = {name: sum(v) / len(v) for name, v in ms.items()}
+    ms = {name: [a.elapsed_time(b) for a, b in ev[name]] for name in ev}
 
     # separate kernel timing pass for the ragged decode alone (for the roofline)
     ra.profile_enable(True)
@@ -576,13 +653,31 @@ def main():
     ra.profile_enable(False)
     n_k, dec_kernel_ms = ra.profile_read("decode")
 
+    # the tiny and the uniform decode batches, timed call by call outside the step
+    for name, t in (("decode_tiny", t_tiny), ("decode_uniform", t_uni)):
+        for _ in range(args.warmup):
+            decode(t)
+        torch.cuda.synchronize()
+        pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                 for _ in range(max(args.steps, 20))]
+        for a, b in pairs:
+            a.record(stream)
+            decode(t)
+            b.record(stream)
+        torch.cuda.synchronize()
+        ms[name] = [a.elapsed_time(b) for a, b in pairs]
+    st = {name: timing_stats(v) for name, v in ms.items()}
+    mean = {name: v["ms_mean"] for name, v in st.items()}
+
     kv_dec = w_dec.kv_bytes()
+    kv_uni = w_uni.kv_bytes()
     kv_grp_unique = w_grp.kv_bytes(unique=True)
     kv_grp_logical = w_grp.kv_bytes()
     kv_ext = w_ext.kv_bytes()
     flops_ext = w_ext.flops()
     dec_gbps = kv_dec / (mean["decode_ragged"] * 1e-3) / 1e9
     kern_gbps = kv_dec / (dec_kernel_ms * 1e-3) / 1e9
+    uni_gbps = kv_uni / (mean["decode_uniform"] * 1e-3) / 1e9
     ext_tflops = flops_ext / (mean["extend_multiturn"] * 1e-3) / 1e12
     ext_kern_tflops = flops_ext / (ext_kernel_ms * 1e-3) / 1e12 if n_ext else None
     grp_s = mean["decode_group_prefix"] * 1e-3
@@ -603,30 +698,39 @@ def main():
         "config": {
             "workload": "step = decode of the agentic ragged batch (B128, Hq96/Hkv8, lognormal median 16K clipped "
                         "1K-64K, page 64; value) + decode with trajectory-group prefix sharing (16x8, shared 4096, "
-                        "private 512-16384, Hq64/Hkv8) + extend (B32, prefix 8K-64K, chunk 64-2048, Hq64/Hkv8)",
+                        "private 512-16384, Hq64/Hkv8) + extend (B32, prefix 8K-64K, chunk 64-2048, Hq64/Hkv8); "
+                        "the tiny (B4, Hq8/Hkv2, 128-512 keys, page 16) and uniform (B64, Hq64/Hkv8, 8192 keys, "
+                        "page 64) decode batches are timed beside the step",
             "decode_batch": w_dec.batch, "decode_sum_kv_tokens": int(w_dec.kv_lens.sum()),
             "decode_kv_bytes": kv_dec, "head_dim": 128, "page_size": 64, "seed": w_dec.seed,
         },
-        "decode_ragged": {
-            "ms_mean": round(mean["decode_ragged"], 4), "ms_median": round(med["decode_ragged"], 4),
+        "decode_ragged": dict(st["decode_ragged"], **{
             "kv_GBps": round(dec_gbps, 2), "hbm_frac": round(dec_gbps / HBM_PEAK_GBPS, 4),
+            "kv_GBps_at_median": round(kv_dec / (st["decode_ragged"]["ms_median"] * 1e-3) / 1e9, 2),
             "tokens_per_s": round(w_dec.batch / (mean["decode_ragged"] * 1e-3), 1),
-        },
-        "decode_group_prefix": {
-            "ms_mean": round(mean["decode_group_prefix"], 4),
+        }),
+        "decode_group_prefix": dict(st["decode_group_prefix"], **{
             "unique_kv_GBps": round(kv_grp_unique / grp_s / 1e9, 2),
             "logical_kv_GBps": round(kv_grp_logical / grp_s / 1e9, 2),
             "hbm_frac_unique": round(kv_grp_unique / grp_s / 1e9 / HBM_PEAK_GBPS, 4),
             "tokens_per_s": round(w_grp.batch / grp_s, 1),
-        },
-        "extend_multiturn": {
-            "ms_mean": round(mean["extend_multiturn"], 4), "tflops": round(ext_tflops, 2),
+        }),
+        "extend_multiturn": dict(st["extend_multiturn"], **{
+            "tflops": round(ext_tflops, 2),
             "mfma_frac": round(ext_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
             "kernel_ms": round(ext_kernel_ms, 4) if n_ext else None,
             "kernel_tflops": round(ext_kern_tflops, 2) if ext_kern_tflops else None,
             "tokens_per_s": round(w_ext.total_q / (mean["extend_multiturn"] * 1e-3), 1),
             "flops": flops_ext, "kv_bytes": kv_ext,
-        },
+        }),
+        "decode_uniform": dict(st["decode_uniform"], **{
+            "kv_bytes": kv_uni, "kv_GBps": round(uni_gbps, 2), "hbm_frac": round(uni_gbps / HBM_PEAK_GBPS, 4),
+            "tokens_per_s": round(w_uni.batch / (mean["decode_uniform"] * 1e-3), 1),
+        }),
+        "decode_tiny": dict(st["decode_tiny"], **{
+            "kv_bytes": w_tiny.kv_bytes(), "bound": "launch latency (time only)",
+            "tokens_per_s": round(w_tiny.batch / (mean["decode_tiny"] * 1e-3), 1),
+        }),
         "roofline": {
             "kernel": "decode_mfma_kernel (ragged 64K decode batch)",
             "bound": "hbm", "achieved": round(kern_gbps, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
@@ -637,8 +741,9 @@ def main():
     }
     # the same ragged decode and extend batches with FP8 E4M3 KV pages (per-KV-head scales):
     # reported beside the bf16 step, not part of it
-    del t_grp
-    torch.cuda.empty_cache()
+    host_inputs = {"decode_tiny": (w_tiny, t_tiny), "decode_uniform": (w_uni, t_uni),
+                   "decode_ragged": (w_dec, t_dec), "decode_group_prefix": (w_grp, t_grp),
+                   "extend_multiturn": (w_ext, t_ext)}
     result["deterministic_decode"] = deterministic_study(args.steps, args.warmup, w_dec, t_dec,
                                                          mean["decode_ragged"])
     result["multi_token_decode"] = mtp_study(args.steps, args.warmup, w_dec, t_dec, mean["decode_ragged"])
@@ -646,22 +751,28 @@ def main():
     result["fp8_kv"] = fp8_study(args.steps, args.warmup, w_dec, w_ext, mean["decode_ragged"],
                                  mean["extend_multiturn"])
     # measured ceilings on this device, beside the specification peaks
-    del t_ext
     torch.cuda.empty_cache()
     buf = torch.ones(4 << 30, dtype=torch.uint8, device=dev)
     read_gbps = ra.diag_read_bandwidth(buf, reps=10)
     del buf
     loop_tflops = ra.diag_mfma_bf16(20000)
     result["ceilings"] = {
-        "hbm_read_GBps": round(read_gbps, 1), "hbm_read_frac_of_spec": round(read_gbps / HBM_PEAK_GBPS, 4),
-        "decode_frac_of_read_ceiling": round(dec_gbps / read_gbps, 4),
+        "read_loop_GBps": round(read_gbps, 1), "read_loop_frac_of_spec": round(read_gbps / HBM_PEAK_GBPS, 4),
+        "decode_over_read_loop": round(dec_gbps / read_gbps, 4),
         "mfma_bf16_loop_TFLOPs": round(loop_tflops, 1),
         "mfma_loop_frac_of_spec": round(loop_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
         "extend_frac_of_mfma_loop": round(ext_tflops / loop_tflops, 4),
     }
     if not args.no_cpu_baseline:
-        log("timing the oracle on host cores ...")
-        result["cpu_baseline"] = cpu_baseline(w_dec, t_dec, args.cpu_budget)
+        log(f"timing the oracle on {HOST_THREADS} host threads ...")
+        per = {}
+        budgets = {"decode_tiny": 1.0, "decode_uniform": 6.0, "decode_ragged": 10.0, "decode_group_prefix": 6.0,
+                   "extend_multiturn": 10.0}
+        for name, (w, t) in host_inputs.items():
+            per[name] = cpu_oracle(w, t, budgets[name] * args.cpu_budget / 15.0)
+            log(f"oracle {name}: {per[name]}")
+        result["cpu_baseline"] = dict(per["decode_ragged"])
+        result["cpu_baseline_per_config"] = per
     print(json.dumps(result), flush=True)
 
 

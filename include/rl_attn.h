@@ -236,18 +236,24 @@ const char* rl_attn_last_error(void);
 
 /* Synchronises `stream`, then returns RL_ERR_DEVICE if any call on this
  * (device, stream) since the last check met an out-of-range page id, length
- * or indptr on the device (those values were clamped), RL_OK otherwise, and
- * clears the error word. */
+ * or indptr on the device (those values were clamped), an invalid FP8 scale,
+ * or work beyond its workspace's capacity, RL_OK otherwise, and clears the
+ * error word. Allocates nothing. */
 int rl_attn_check_device_errors(void* stream);
 
 /* Grows this (device, stream)'s workspace to at least `bytes` now, so later
  * calls (e.g. under stream capture) need no allocation. */
 int rl_attn_reserve_workspace(size_t bytes, void* stream);
 
-/* Workspace bytes a decode / extend call with these sizes may need (for a
- * decode with n query tokens per sequence pass num_q_heads = n * Hq). */
+/* Workspace bytes a decode / extend call with these sizes may need on the
+ * current device, for rl_attn_reserve_workspace ahead of stream capture.
+ * Decode: query_tokens query tokens per sequence (1 for a 3-D q, n for q
+ * [B, n, Hq, 128]) and split_tokens the opts.split_tokens the call will pass
+ * (0 = automatic); the size covers bf16 and FP8 pages, prefix sharing on or off
+ * and the deterministic mode. Returns 0 for sizes a call would reject. */
 size_t rl_attn_decode_workspace_size(int64_t batch, int64_t num_q_heads, int64_t num_kv_heads,
-                                     int64_t max_pages, int64_t page_size);
+                                     int64_t max_pages, int64_t page_size, int64_t query_tokens,
+                                     int32_t split_tokens);
 size_t rl_attn_extend_workspace_size(int64_t batch, int64_t total_q, int64_t num_q_heads,
                                      int64_t num_kv_heads, int64_t max_pages, int64_t page_size);
 

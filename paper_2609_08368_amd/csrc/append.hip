@@ -144,7 +144,7 @@ __global__ __launch_bounds__(kAppendThreads) void append_kernel(AppendArgs a) {
       *reinterpret_cast<bf16x8*>((__bf16*)a.v + vo) = vx[j];
     } else {
       const float ks = a.k_scale[g * a.ks_s], vs = a.v_scale[g * a.vs_s];
-      if (!(ks > 0.f && ks < __builtin_huge_valf()) || !(vs > 0.f && vs < __builtin_huge_valf())) {
+      if (!scale_ok(ks) || !scale_ok(vs)) {
         atomicOr(a.err, kErrScale);
         continue;
       }

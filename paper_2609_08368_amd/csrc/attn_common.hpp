@@ -151,6 +151,12 @@ __device__ __forceinline__ bf16x8 load_kv8(const char* p) {
   return kv_to_bf16x8<kFp8>(load_kv_raw<kFp8>(p));
 }
 
+// A dequantisation scale is usable when it is positive, non-zero and finite:
+// its bit pattern lies in [1, 0x7f7fffff] (smallest positive subnormal up to
+// the largest finite float). Tested on the bits rather than by comparisons,
+// since the device code is compiled assuming no NaN operands.
+__device__ __forceinline__ bool scale_ok(float s) { return (__float_as_uint(s) - 1u) < 0x7f7fffffu; }
+
 // Dequantisation scales of KV head g (1 for bf16 pages); *bad is set when a
 // scale is not positive and finite.
 struct KvScales {
@@ -162,7 +168,7 @@ __device__ __forceinline__ KvScales kv_scales(const KV& kv, int g, int* bad) {
     return {1.f, 1.f};
   } else {
     const float ks = kv.k_scale[g * kv.ks_s], vs = kv.v_scale[g * kv.vs_s];
-    if (!(ks > 0.f && ks < __builtin_huge_valf()) || !(vs > 0.f && vs < __builtin_huge_valf())) *bad = 1;
+    if (!scale_ok(ks) || !scale_ok(vs)) *bad = 1;
     return {ks, vs};
   }
 }

@@ -59,7 +59,7 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
   const bool small = a.B <= kGroupMax;
   const bool grouping = a.group_cap >= 2 && small;
   const uint32_t bt_sj = (uint32_t)a.kv.bt_sj;
-  int bad = 0;
+  int bad = 0, cap_bad = 0;
 
   if (grouping)
     for (int i = tid; i < (1 << kHashBits); i += nthr) {
@@ -222,10 +222,13 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
     int slot_tot;
     const int slot_base = slot_off + block_exclusive_scan(nslots, &slot_tot, wave_tot);
     if (b < a.B) {
+      // a sequence whose slots do not fit writes nothing (the host sizes the
+      // workspace so that this never happens; it is reported, not raced)
       const bool fits = slot_base + nslots <= a.max_slots;
-      a.ws.nparts[b] = empty ? -1 : (fits ? nslots : 0);
+      if (!fits) cap_bad = 1;
+      a.ws.nparts[b] = empty ? -1 : (fits ? nslots : -2);
       a.ws.base[b] = slot_base;
-      a.ws.seqs[b] = make_int4(S, direct || !fits ? -1 : slot_base + nsh, L, fits ? 1 : 0);
+      a.ws.seqs[b] = make_int4(S, !fits ? kSlotDropped : (direct ? kSlotDirect : slot_base + nsh), L, fits ? 1 : 0);
       if (S > 0) {
         const int lead = sLead[b];
         int rank = 0;
@@ -249,8 +252,12 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
     int tot;
     const int base = sitem_off + block_exclusive_scan(sg < n_sg ? info.w : 0, &tot, wave_tot);
     if (sg < n_sg)
-      for (int s = 0; s < info.w; ++s)
-        if (base + s < a.max_items) a.ws.sitems[base + s] = make_int4(sg, s * C, min(info.z, (s + 1) * C), s);
+      for (int s = 0; s < info.w; ++s) {
+        if (base + s < a.max_items)
+          a.ws.sitems[base + s] = make_int4(sg, s * C, min(info.z, (s + 1) * C), s);
+        else
+          cap_bad = 1;
+      }
     sitem_off += tot;
   }
   if (tid == 0) {
@@ -260,6 +267,7 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
     a.ws.hdr[3] = n_sg;
   }
   if (bad) atomicOr(a.ws.err, kErrLen);
+  if (cap_bad) atomicOr(a.ws.err, kErrCapacity);
 }
 
 // Writes a finished (o, l, m) for one query head: directly to out/lse, or as
@@ -297,7 +305,7 @@ __device__ __forceinline__ void for_each_piece(const DecodeArgs& a, int w, F&& f
     const long long p0 = a.ws.pref[b], p1 = a.ws.pref[b + 1];
     if (p1 <= x) continue;
     const long long e = p1 < x_end ? p1 : x_end;
-    const int4 sq = a.ws.seqs[b];   // (S, first private slot or -1, L, slots fit)
+    const int4 sq = a.ws.seqs[b];   // (S, first private slot or a slot marker, L, slots fit)
     int slot = sq.y;
     if (slot >= 0 && x > p0) slot += w - (int)(((p0 + 1) * n + W - 1) / W) + 1;
     const int t_end = sq.x + (int)((e - p0) * kTile);
@@ -532,8 +540,8 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
 
   const HeadResult res = finish(m_run, group_sum(l_run));
   const float inv = res.inv * dq.v;            // the V dequantisation scale
-  if (col_ok) {
-    if (slot < 0) {
+  if (col_ok && slot != kSlotDropped) {
+    if (slot == kSlotDirect) {
       if (a.out_f32) {
         float* op = (float*)a.out + (int64_t)b * a.out_sb + (int64_t)h * a.out_sh + 4 * grp;
 #pragma unroll
@@ -620,8 +628,8 @@ __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
   for (int i = 0; i < 8; ++i) acc[i] = group_sum(acc[i] * w);
   const HeadResult res = finish(M, l_tot);
   const float inv = res.inv * dq.v;
-  if (grp == 0) {
-    if (slot < 0) {
+  if (grp == 0 && slot != kSlotDropped) {
+    if (slot == kSlotDirect) {
       if (a.out_f32) {
         float* op = (float*)a.out + (int64_t)b * a.out_sb + (int64_t)h * a.out_sh + c16 * 8;
 #pragma unroll
@@ -707,9 +715,9 @@ __global__ __launch_bounds__(kMultiWaves * 64, 2) void decode_multi_kernel(Decod
                                           limit, qv, lds, o, m_run, l_run, bad, t_begin,
                                           rb * kMultiWaves * kWaveRows + wave * kWaveRows < rows);
     const HeadResult res = finish(m_run, sum_l32(l_run));
-    if (row_ok) {
+    if (row_ok && slot != kSlotDropped) {
       const float inv = res.inv * dq.v;
-      if (slot < 0) {
+      if (slot == kSlotDirect) {
         const int64_t oo = (int64_t)b * a.out_sb + (int64_t)tok * a.out_st + (int64_t)head * a.out_sh;
         if (a.out_f32)
           store_o_row((float*)a.out + oo, o, inv);
@@ -778,7 +786,7 @@ __global__ __launch_bounds__(kPrefixWaves * 64, 2) void prefix_kernel(DecodeArgs
     const HeadResult res = finish(m_run, sum_l32(l_run));
     if (row_ok) {
       const int slot = a.ws.base[b] + split;
-      if (slot < a.max_slots) {
+      if (a.ws.seqs[b].w) {                        // the member's slots fit the workspace
         const int64_t row = (int64_t)slot * a.Hv + (int64_t)tok * a.Hq + head;
         store_o_row(a.ws.part_o + row * kHeadDim, o, res.inv * dq.v);
         if (lane < 32) a.ws.part_lse[row] = res.lse;
@@ -842,8 +850,10 @@ __global__ __launch_bounds__(64) void combine_kernel(DecodeArgs a) {
   const int tok = hv / a.Hq, h = hv - tok * a.Hq;
   const int n = a.ws.nparts[b];
   if (n == 0) return;     // written directly by its only piece
-  float r[2] = {0.f, 0.f}, lse_v = kNegInf;   // an empty sequence (n < 0): zeros, -inf
-  if (n > 0) {
+  float r[2] = {0.f, 0.f}, lse_v = kNegInf;   // an empty sequence (n == -1): zeros, -inf
+  if (n == -2) {          // its slots did not fit the workspace (reported as kErrCapacity)
+    r[0] = r[1] = lse_v = __uint_as_float(0x7fc00000u);   // a quiet NaN
+  } else if (n > 0) {
     const int base = a.ws.base[b];
     merge_parts(a.ws.part_o + ((int64_t)base * a.Hv + hv) * kHeadDim, (int64_t)a.Hv * kHeadDim,
                 a.ws.part_lse + (int64_t)base * a.Hv + hv, a.Hv, n, r, &lse_v);

@@ -134,7 +134,10 @@ __global__ __launch_bounds__(1024) void plan_extend_kernel(ExtendArgs a) {
           }
           const int i0 = (nt - 1 - j) * a.tile_tokens;
           const int cnt = min(a.tile_tokens, r.n - i0);
-          if (idx < a.max_items) a.ws.items[idx] = make_int4(b, i0, cnt, g | (hb << 16));
+          if (idx < a.max_items)
+            a.ws.items[idx] = make_int4(b, i0, cnt, g | (hb << 16));
+          else
+            bad |= kErrCapacity;     // the host sizing rules this out; reported, never dropped silently
         }
       }
     }

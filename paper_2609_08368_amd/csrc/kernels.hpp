@@ -13,7 +13,14 @@ enum DeviceError : int {
   kErrIndptr = 4,    // qo_indptr not non-decreasing within [0, total_q] (clamped)
   kErrKvShort = 8,   // kv_lens[b] < chunk length (clamped up)
   kErrScale = 16,    // an FP8 dequantisation scale that is not positive and finite
+  kErrCapacity = 32, // the work of a call exceeded its workspace's capacity (affected
+                     // outputs are NaN or left unwritten; the host sizing rules out this case)
 };
+
+// Slot markers of a decode piece: its result goes straight to out/lse, or
+// nowhere (its sequence's partial slots did not fit the workspace).
+constexpr int kSlotDirect = -1;
+constexpr int kSlotDropped = -2;
 
 // Paged KV cache + block table, shared by decode and extend.
 struct PagedKV {
@@ -39,13 +46,16 @@ struct PagedKV {
 // every member of one sub-group (at most 128 query rows). Partial results
 // live in "slots"; sequence b owns slots base[b] .. base[b] + nparts[b] - 1:
 // its shared splits, then its private pieces in key order (nparts[b] == 0:
-// one piece, written directly; -1: an empty sequence, written by the combine).
+// one piece, written directly; -1: an empty sequence, written by the combine;
+// -2: its slots did not fit, so the combine writes NaN and the error word
+// records kErrCapacity).
 struct DecodePlanWs {
   int* hdr;        // [0] split tokens C of shared keys, [1] workers, [2] shared items, [3] sub-groups
   int* nparts;     // [B]
   int* base;       // [B]
   long long* pref; // [B + 1] prefix sums of private keys
-  int4* seqs;      // [B] (shared keys S, slot of the first private piece or -1 for a direct write, L, 0)
+  int4* seqs;      // [B] (shared keys S, slot of the first private piece, kSlotDirect or kSlotDropped, L,
+                   //      1 if the sequence's slots fit the workspace)
   int4* sitems;    // [max_items] (sub-group, first key, end key, split index)
   int4* sgroups;   // [B] (sequence whose block table is read, members, shared keys, shared splits)
   int* sg_members; // [B * group_cap] member sequences of each sub-group
@@ -160,6 +170,7 @@ struct KernelTimer {
 };
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream, KernelTimer* timer);
+
 // Measurement aids (see rl_attn_diag.h): a grid-stride read of `bytes` and a
 // register-only bf16 MFMA loop.
 hipError_t launch_diag_read(const void* buf, size_t bytes, unsigned* sink, int cus, hipStream_t stream);

@@ -231,6 +231,21 @@ int acquire_ws(hipStream_t st, size_t need, Workspace** out) {
   return RL_OK;
 }
 
+// A call's workspace: this (device, stream)'s library workspace (grown with
+// hipMalloc) and its error word.
+struct WsView {
+  char* ptr;
+  int* err;
+};
+
+int get_ws(hipStream_t st, size_t need, WsView* v) {
+  Workspace* w = nullptr;
+  RL_TRY(acquire_ws(st, need, &w));
+  v->ptr = static_cast<char*>(w->ptr);
+  v->err = w->err;
+  return RL_OK;
+}
+
 // ------------------------------------------------------------ kernel timing
 struct Profiler {
   std::mutex mu;
@@ -268,11 +283,15 @@ void prof_commit(int kind, rl::KernelTimer* t) {
 }
 
 // ------------------------------------------------------------------- decode
+constexpr int64_t kMinSplitKeys = 256;   // the planner's smallest automatic split of shared keys
+
 // Capacities (see the planner): with split size C and T = sum(L) / C,
 // Private pieces <= workers + B, shared items <= T + B, partial slots <=
 // workers + T + 2B. An automatic shared split C keeps T at or below the target
-// item count; a forced C bounds T by B * ceil(max_pages * P / C) and lets the
-// private pass use up to that many workers of C keys.
+// item count, and C >= kMinSplitKeys keeps it at or below
+// B * ceil(max_pages * P / kMinSplitKeys); a forced C bounds T by
+// B * ceil(max_pages * P / C) and lets the private pass use up to that many
+// workers of C keys.
 struct DecodeLayout {
   int max_items, max_slots, max_workers, group_cap;
   size_t off_nparts, off_base, off_pref, off_seqs, off_sitems, off_sgroups, off_members, off_po, off_pl, total;
@@ -311,18 +330,23 @@ int workers_per_cu(int64_t Hq, int64_t Hkv, bool fp8, int n_tok) {
   return n;
 }
 
-// n_tok query tokens per sequence: partial rows and group sizes count n_tok * Hq
-// rows per sequence (the layout of (Hq, n_tok) is at most that of (n_tok * Hq, 1))
-DecodeLayout decode_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t max_pages, int64_t P, int split, int cus,
-                           bool prefix_share, bool fp8, int n_tok = 1) {
+// Workspace layout of a decode call with n_tok query tokens per sequence (partial
+// rows and group sizes count n_tok * Hq rows per sequence) on `cus` compute units
+// holding `wpc` private-pass workers each.
+DecodeLayout decode_layout_with(int64_t B, int64_t Hq, int64_t Hkv, int64_t max_pages, int64_t P, int split,
+                                int cus, int wpc, bool prefix_share, int n_tok) {
   DecodeLayout L{};
   const int64_t R = Hq / std::max<int64_t>(1, Hkv);
   const int64_t rows_kv = R * n_tok;              // query rows of one KV head
   const int64_t Hv = Hq * n_tok;
   const int64_t max_tokens = max_pages * P;
+  // an automatic split is at least kMinSplitKeys keys, so a sequence has at most
+  // ceil(max_tokens / kMinSplitKeys) shared splits whatever the item target
   const int64_t T = split > 0 ? B * std::max<int64_t>(1, (max_tokens + split - 1) / split)
-                              : (int64_t)target_items_for(Hq, Hkv, cus);
-  const int64_t workers = split > 0 ? T : (int64_t)cus * workers_per_cu(Hq, Hkv, fp8, n_tok);
+                              : std::min<int64_t>(target_items_for(Hq, Hkv, cus),
+                                                  B * std::max<int64_t>(1, (max_tokens + kMinSplitKeys - 1) /
+                                                                               kMinSplitKeys));
+  const int64_t workers = split > 0 ? T : (int64_t)cus * wpc;
   L.max_items = (int)std::min<int64_t>(T + B, INT32_MAX / 2);
   L.max_workers = (int)std::min<int64_t>(std::max<int64_t>(1, workers), INT32_MAX / 64);
   L.max_slots = (int)std::min<int64_t>(L.max_workers + T + 2 * B, INT32_MAX / 2);
@@ -348,6 +372,12 @@ DecodeLayout decode_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t max_pages
   off += align256((size_t)L.max_slots * Hv * 4);
   L.total = off;
   return L;
+}
+
+DecodeLayout decode_layout(int64_t B, int64_t Hq, int64_t Hkv, int64_t max_pages, int64_t P, int split, int cus,
+                           bool prefix_share, bool fp8, int n_tok) {
+  return decode_layout_with(B, Hq, Hkv, max_pages, P, split, cus, workers_per_cu(Hq, Hkv, fp8, n_tok),
+                            prefix_share, n_tok);
 }
 
 // One dequantisation scale per KV head: [Hkv] f32. The values are checked on
@@ -484,9 +514,9 @@ size_t extend_ws_bytes(int64_t B, int64_t total_q, int64_t Hkv, int64_t R, int* 
 int run_extend(rl::ExtendArgs& a, hipStream_t st, int prof_kind) {
   int max_items = 0;
   const size_t bytes = extend_ws_bytes(a.B, a.total_q, a.Hkv, a.R, &max_items);
-  Workspace* w = nullptr;
-  RL_TRY(acquire_ws(st, bytes, &w));
-  char* base = static_cast<char*>(w->ptr);
+  WsView w{};
+  RL_TRY(get_ws(st, bytes, &w));
+  char* base = w.ptr;
   const ExtendShape s = extend_shape(a.R);
   a.rows_head = s.rows_head;
   a.tile_tokens = s.tile_tokens;
@@ -494,7 +524,7 @@ int run_extend(rl::ExtendArgs& a, hipStream_t st, int prof_kind) {
   a.max_items = max_items;
   a.ws.hdr = reinterpret_cast<int*>(base);
   a.ws.items = reinterpret_cast<int4*>(base + 256);
-  a.ws.err = w->err;
+  a.ws.err = w.err;
   rl::KernelTimer slot;
   rl::KernelTimer* timer = prof_timer(&slot, st);
   hipError_t e = rl::launch_extend(a, st, timer);
@@ -583,9 +613,9 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   const int cus = device_cus(dev);
   const DecodeLayout lay = decode_layout(B, Hq, Hkv, a.kv.max_pages, a.kv.page_size, o.split_tokens, cus,
                                          o.prefix_share == RL_PREFIX_AUTO, kv_dtype == RL_FP8_E4M3, (int)n_tok);
-  Workspace* w = nullptr;
-  RL_TRY(acquire_ws(st, lay.total, &w));
-  char* base = static_cast<char*>(w->ptr);
+  WsView w{};
+  RL_TRY(get_ws(st, lay.total, &w));
+  char* base = w.ptr;
   a.q = q->data;
   a.q_sb = q->strides[0];
   a.q_sh = q->strides[hd];
@@ -626,7 +656,7 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   a.ws.sg_members = reinterpret_cast<int*>(base + lay.off_members);
   a.ws.part_o = reinterpret_cast<float*>(base + lay.off_po);
   a.ws.part_lse = reinterpret_cast<float*>(base + lay.off_pl);
-  a.ws.err = w->err;
+  a.ws.err = w.err;
   rl::KernelTimer slot;
   rl::KernelTimer* timer = prof_timer(&slot, st);
   e = rl::launch_decode(a, st, timer);
@@ -892,15 +922,29 @@ const char* rl_attn_last_error(void) { return g_err.c_str(); }
 
 int rl_attn_check_device_errors(void* stream) {
   hipStream_t st = static_cast<hipStream_t>(stream);
-  Workspace* w = nullptr;
-  RL_TRY(acquire_ws(st, 0, &w));
-  hipError_t e = hipStreamSynchronize(st);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  // the error word of this stream's workspace, if a call made one (none is
+  // created here)
+  int* words[1] = {nullptr};
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_ws.find({dev, st});
+    if (it != g_ws.end()) words[0] = it->second.err;
+  }
+  e = hipStreamSynchronize(st);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
   int word = 0;
-  e = hipMemcpy(&word, w->err, sizeof(int), hipMemcpyDeviceToHost);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpy");
-  e = hipMemset(w->err, 0, sizeof(int));
-  if (e != hipSuccess) return hip_fail(e, "hipMemset");
+  for (int* p : words) {
+    if (!p) continue;
+    int wv = 0;
+    e = hipMemcpy(&wv, p, sizeof(int), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy");
+    e = hipMemset(p, 0, sizeof(int));
+    if (e != hipSuccess) return hip_fail(e, "hipMemset");
+    word |= wv;
+  }
   if (word) {
     std::string what;
     if (word & rl::kErrLen) what += " length-out-of-range";
@@ -908,6 +952,7 @@ int rl_attn_check_device_errors(void* stream) {
     if (word & rl::kErrIndptr) what += " qo_indptr-invalid";
     if (word & rl::kErrKvShort) what += " kv_lens-shorter-than-chunk";
     if (word & rl::kErrScale) what += " dequant-scale-invalid";
+    if (word & rl::kErrCapacity) what += " workspace-capacity-exceeded";
     return fail(RL_ERR_DEVICE, "device-side input errors (values were clamped):%s", what.c_str());
   }
   return RL_OK;
@@ -919,18 +964,21 @@ int rl_attn_reserve_workspace(size_t bytes, void* stream) {
 }
 
 size_t rl_attn_decode_workspace_size(int64_t batch, int64_t num_q_heads, int64_t num_kv_heads, int64_t max_pages,
-                                     int64_t page_size) {
-  if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0) return 0;
+                                     int64_t page_size, int64_t query_tokens, int32_t split_tokens) {
+  if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0 || max_pages < 0 || page_size <= 0) return 0;
+  if (query_tokens < 1 || query_tokens > 64 || split_tokens < 0 || split_tokens % 64 != 0) return 0;
+  if (batch > (1 << 22) || num_q_heads > 4096 || batch * query_tokens * num_q_heads > INT32_MAX) return 0;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess) cus = device_cus(dev);
+  const int split = split_tokens ? split_tokens : env().split_tokens;
   // bf16 and FP8 pages may keep different numbers of workers resident, and a
   // deterministic decode uses the extend work list: the largest of the three
   int mi = 0;
   const int64_t R = num_q_heads / num_kv_heads;
-  size_t total = R >= 1 ? extend_ws_bytes(batch, batch, num_kv_heads, R, &mi) : 0;
+  size_t total = R >= 1 ? extend_ws_bytes(batch, batch * query_tokens, num_kv_heads, R, &mi) : 0;
   for (bool fp8 : {false, true})
-    total = std::max(total, decode_layout(batch, num_q_heads, num_kv_heads, max_pages, page_size, env().split_tokens,
-                                          cus, env().prefix_share == RL_PREFIX_AUTO, fp8)
+    total = std::max(total, decode_layout(batch, num_q_heads, num_kv_heads, max_pages, page_size, split, cus,
+                                          true, fp8, (int)query_tokens)
                                 .total);
   return total;
 }
@@ -1018,6 +1066,41 @@ int rl_attn_diag_mfma_bf16(int64_t iters, double* tflop_per_s, void* stream) {
   (void)hipEventDestroy(b);
   if (e != hipSuccess) return hip_fail(e, "diag_mfma_bf16");
   *tflop_per_s = ms > 0.f ? rl::diag_mfma_flops((int)iters, cus) / (ms * 1e-3) / 1e12 : 0.0;
+  return RL_OK;
+}
+
+int rl_attn_diag_decode_capacity(int64_t batch, int64_t num_q_heads, int64_t num_kv_heads, int64_t max_pages,
+                                 int64_t page_size, int64_t query_tokens, int32_t split_tokens, int32_t prefix_share,
+                                 int32_t cus, int32_t workers_per_cu, int64_t* out) {
+  if (!out) return fail(RL_ERR_INVALID_ARG, "diag_decode_capacity: out is NULL");
+  if (batch <= 0 || num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads != 0 || max_pages < 0 ||
+      page_size <= 0 || query_tokens < 1 || query_tokens > 64 || split_tokens < 0 || split_tokens % 64 != 0 ||
+      cus < 1 || workers_per_cu < 1)
+    return fail(RL_ERR_INVALID_ARG, "diag_decode_capacity: invalid sizes");
+  const DecodeLayout L = decode_layout_with(batch, num_q_heads, num_kv_heads, max_pages, page_size, split_tokens, cus,
+                                            workers_per_cu, prefix_share != 0, (int)query_tokens);
+  out[0] = L.max_items;
+  out[1] = L.max_slots;
+  out[2] = L.max_workers;
+  out[3] = L.group_cap;
+  out[4] = target_items_for(num_q_heads, num_kv_heads, cus);
+  out[5] = 2 * (int64_t)cus;
+  out[6] = (int64_t)L.total;
+  return RL_OK;
+}
+
+int rl_attn_diag_extend_capacity(int64_t batch, int64_t total_q, int64_t num_q_heads, int64_t num_kv_heads,
+                                 int64_t* out) {
+  if (!out) return fail(RL_ERR_INVALID_ARG, "diag_extend_capacity: out is NULL");
+  if (batch <= 0 || total_q < 0 || num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads != 0)
+    return fail(RL_ERR_INVALID_ARG, "diag_extend_capacity: invalid sizes");
+  int mi = 0;
+  (void)extend_ws_bytes(batch, total_q, num_kv_heads, num_q_heads / num_kv_heads, &mi);
+  const ExtendShape sh = extend_shape(num_q_heads / num_kv_heads);
+  out[0] = mi;
+  out[1] = sh.rows_head;
+  out[2] = sh.tile_tokens;
+  out[3] = sh.head_blocks;
   return RL_OK;
 }
 

@@ -71,7 +71,7 @@ def lib() -> ctypes.CDLL:
         L.rl_attn_last_error.restype = ctypes.c_char_p
         L.rl_attn_check_device_errors.argtypes = [vp]
         L.rl_attn_reserve_workspace.argtypes = [ctypes.c_size_t, vp]
-        L.rl_attn_decode_workspace_size.argtypes = [ctypes.c_int64] * 5
+        L.rl_attn_decode_workspace_size.argtypes = [ctypes.c_int64] * 6 + [ctypes.c_int32]
         L.rl_attn_decode_workspace_size.restype = ctypes.c_size_t
         L.rl_attn_extend_workspace_size.argtypes = [ctypes.c_int64] * 6
         L.rl_attn_extend_workspace_size.restype = ctypes.c_size_t
@@ -81,11 +81,14 @@ def lib() -> ctypes.CDLL:
         dp = ctypes.POINTER(ctypes.c_double)
         L.rl_attn_diag_read_bandwidth.argtypes = [vp, ctypes.c_int64, ctypes.c_int32, dp, vp]
         L.rl_attn_diag_mfma_bf16.argtypes = [ctypes.c_int64, dp, vp]
+        i64p = ctypes.POINTER(ctypes.c_int64)
+        L.rl_attn_diag_decode_capacity.argtypes = [ctypes.c_int64] * 6 + [ctypes.c_int32] * 4 + [i64p]
+        L.rl_attn_diag_extend_capacity.argtypes = [ctypes.c_int64] * 4 + [i64p]
         for name in ("rl_attn_decode", "rl_attn_extend", "rl_attn_decode_ex", "rl_attn_extend_ex",
                      "rl_attn_decode_fp8", "rl_attn_extend_fp8", "rl_attn_append_kv", "rl_attn_append_kv_fp8",
                      "rl_attn_merge", "rl_attn_check_device_errors", "rl_attn_reserve_workspace",
                      "rl_attn_profile_enable", "rl_attn_profile_read", "rl_attn_diag_read_bandwidth",
-                     "rl_attn_diag_mfma_bf16"):
+                     "rl_attn_diag_mfma_bf16", "rl_attn_diag_decode_capacity", "rl_attn_diag_extend_capacity"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -260,9 +263,11 @@ def reserve_workspace(nbytes: int, stream=None):
     _check(lib().rl_attn_reserve_workspace(ctypes.c_size_t(nbytes), _stream(stream)))
 
 
-def decode_workspace_size(batch: int, num_q_heads: int, num_kv_heads: int, max_pages: int, page_size: int) -> int:
-    """Workspace bytes a decode call may need (n query tokens per sequence: pass n * Hq heads)."""
-    return int(lib().rl_attn_decode_workspace_size(batch, num_q_heads, num_kv_heads, max_pages, page_size))
+def decode_workspace_size(batch: int, num_q_heads: int, num_kv_heads: int, max_pages: int, page_size: int,
+                          query_tokens: int = 1, split_tokens: int = 0) -> int:
+    """Workspace bytes a decode call may need (``query_tokens`` per sequence, the call's ``split_tokens``)."""
+    return int(lib().rl_attn_decode_workspace_size(batch, num_q_heads, num_kv_heads, max_pages, page_size,
+                                                   query_tokens, split_tokens))
 
 
 def extend_workspace_size(batch: int, total_q: int, num_q_heads: int, num_kv_heads: int, max_pages: int,
@@ -300,3 +305,20 @@ def diag_mfma_bf16(iters: int = 20000, stream=None) -> float:
     t = ctypes.c_double(0.0)
     _check(lib().rl_attn_diag_mfma_bf16(iters, ctypes.byref(t), _stream(stream)))
     return t.value
+
+
+def diag_decode_capacity(batch, num_q_heads, num_kv_heads, max_pages, page_size, query_tokens=1, split_tokens=0,
+                         prefix_share=True, cus=256, workers_per_cu=1) -> dict:
+    """Workspace capacities a decode call would be given (host arithmetic only)."""
+    out = (ctypes.c_int64 * 7)()
+    _check(lib().rl_attn_diag_decode_capacity(batch, num_q_heads, num_kv_heads, max_pages, page_size, query_tokens,
+                                              split_tokens, int(bool(prefix_share)), cus, workers_per_cu, out))
+    keys = ("max_items", "max_slots", "max_workers", "group_cap", "target_items", "prefix_grid", "bytes")
+    return dict(zip(keys, (int(x) for x in out)))
+
+
+def diag_extend_capacity(batch, total_q, num_q_heads, num_kv_heads) -> dict:
+    """Work-unit capacity of an extend call (host arithmetic only)."""
+    out = (ctypes.c_int64 * 4)()
+    _check(lib().rl_attn_diag_extend_capacity(batch, total_q, num_q_heads, num_kv_heads, out))
+    return dict(zip(("max_items", "rows_head", "tile_tokens", "head_blocks"), (int(x) for x in out)))

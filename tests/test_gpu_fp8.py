@@ -170,15 +170,50 @@ def test_fp8_extend_full_size_sampled():
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("bad", [-1.0, 0.0, float("inf"), float("nan")])
-def test_fp8_invalid_scale_is_reported(bad):
-    """A scale that is not positive and finite is flagged in the device error word."""
-    w = wl.custom(97, "decode", [40, 70], hq=8, hkv=2, page_size=16)
-    H.say(f"fp8 bad scale {bad}")
+BAD_SCALES = [-1.0, 0.0, -0.0, float("inf"), float("-inf"), float("nan"), -float("nan")]
+SCALE_CALLS = ["decode", "decode_multi_token", "decode_deterministic", "decode_group_prefix", "extend", "append"]
+
+
+@pytest.mark.parametrize("call", SCALE_CALLS)
+@pytest.mark.parametrize("bad", BAD_SCALES, ids=[repr(b) for b in BAD_SCALES])
+def test_fp8_invalid_scale_is_reported(call, bad):
+    """A scale that is not positive and finite (NaN of either sign included) is flagged in
+    the device error word by every kernel that reads one, whatever the compiler assumes about
+    NaN operands; a valid scale raises no error."""
+    if call in ("decode", "decode_deterministic", "append"):
+        w = wl.custom(97, "decode", [40, 70], hq=8, hkv=2, page_size=16)
+    elif call == "decode_group_prefix":
+        w = wl.custom(98, "decode", [64 + 5, 64 + 9, 64 + 30], hq=8, hkv=2, page_size=16, group_size=3,
+                      shared_tokens=64)
+    else:
+        w = wl.custom(99, "extend", [40, 70], q_lens=[3, 3], hq=8, hkv=2, page_size=16)
+    H.say(f"fp8 bad scale {bad} {call}")
     t = wl.materialize_fp8(w, DEV)
+
+    def go():
+        if call == "decode":
+            H.run_decode(w, t)
+        elif call == "decode_deterministic":
+            H.run_decode(w, t, deterministic=True)
+        elif call == "decode_group_prefix":
+            H.run_decode(w, t, split_tokens=64)
+        elif call == "decode_multi_token":
+            q = t["q"].view(w.batch, 3, w.hq, 128)
+            ra.decode_fp8(q, t["k_pages"], t["v_pages"], t["k_scale"], t["v_scale"], t["block_table"],
+                          t["kv_lens"], t["scale"], out=torch.empty_like(q))
+        elif call == "extend":
+            H.run_extend(w, t)
+        else:
+            rows = torch.randn((w.batch, w.hkv, 128), device=DEV).to(torch.bfloat16)
+            ra.append_kv_fp8(rows, rows, torch.arange(w.batch + 1, dtype=torch.int32, device=DEV),
+                             t["block_table"], t["kv_lens"], t["k_pages"], t["v_pages"], t["k_scale"], t["v_scale"])
+
     ra.check_device_errors()
-    t["v_scale"][1] = bad
-    H.run_decode(w, t)
+    go()
+    ra.check_device_errors()    # valid scales: no error
+    which = "k_scale" if call in ("extend", "decode_group_prefix") else "v_scale"
+    t[which][1] = bad
+    go()
     with pytest.raises(ra.RlAttnError) as e:
         ra.check_device_errors()
     assert e.value.status == "RL_ERR_DEVICE" and "dequant-scale-invalid" in str(e.value)

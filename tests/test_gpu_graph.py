@@ -38,7 +38,8 @@ def _replay_and_compare(g, q_static, fresh, eager, outs, what, oracle=None):
 
 @pytest.mark.parametrize("fp8", [False, True])
 @pytest.mark.parametrize("n", [1, 4])
-def test_decode_graph_replays_equal_eager(fp8, n):
+@pytest.mark.parametrize("warm", [True, False], ids=["warm", "reserve_only"])
+def test_decode_graph_replays_equal_eager(fp8, n, warm):
     lens = [700, 4, 3000, 129, 64]
     w = wl.custom(401, "extend" if n > 1 else "decode", lens, q_lens=[n] * len(lens) if n > 1 else None,
                   hq=16, hkv=2, page_size=64)
@@ -67,12 +68,18 @@ def test_decode_graph_replays_equal_eager(fp8, n):
         return out, lse
 
     s = torch.cuda.Stream()
-    ra.reserve_workspace(ra.decode_workspace_size(B, n * hq, w.hkv, t["block_table"].shape[1], w.page_size), stream=s)
+    ra.reserve_workspace(ra.decode_workspace_size(B, hq, w.hkv, t["block_table"].shape[1], w.page_size,
+                                                  query_tokens=n), stream=s)
     q_static = fresh(99)
     out = torch.empty(shape, dtype=torch.bfloat16, device=DEV)
     lse = torch.empty(shape[:-1], dtype=torch.float32, device=DEV)
-    with torch.cuda.stream(s):
-        call(q_static, out, lse, stream=s)        # warm-up on the capture stream
+    if warm:
+        with torch.cuda.stream(s):
+            call(q_static, out, lse, stream=s)    # warm-up on the capture stream
+    else:
+        # the capture stream's first call is the captured one: its reserved
+        # workspace must suffice (an eager call elsewhere loads the kernels)
+        call(q_static, out, lse)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=s):
