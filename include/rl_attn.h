@@ -163,6 +163,27 @@ int rl_attn_extend_ex(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_t
                       float scale, rl_tensor* out, rl_tensor* lse_out, const rl_attn_opts* opts,
                       void* stream);
 
+/* Allocation-free decode, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc). Arguments, results and options are those of rl_attn_decode_ex
+ * (bf16 pages), and it runs the same kernels; its workspace is instead a
+ * statically allocated array of 128 MiB per device (its first 256 bytes are an
+ * error word), held by every device the library runs on until the process ends.
+ * The call makes no hipMalloc, hipFree or other allocating call.
+ * Limit: a call whose workspace would exceed 128 MiB - 256 B is rejected with
+ * RL_ERR_WORKSPACE before any launch (the workspace grows with the batch, the
+ * query heads and query tokens per sequence, and, with a forced split, with
+ * max_pages * page_size / split_tokens; e.g. batch 128 with 96 query heads, one
+ * token, automatic split, fits). Every call on a device shares that device's
+ * array, which keeps the last call's contents: calls that overlap on one
+ * device (e.g. on two streams) race; order them on one stream. Device-side
+ * input errors of these calls go to the array's error word, which
+ * rl_attn_check_device_errors reports on any stream of the device (after
+ * synchronising only the stream it is given). */
+int rl_attn_decode_noalloc(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages,
+                           const rl_tensor* block_table, const rl_tensor* seq_lens, float scale,
+                           rl_tensor* out, rl_tensor* lse_out, const rl_attn_opts* opts, void* stream);
+
 /* FP8 KV pages (paper: the rollout engine of the case study, section "Case
  * Study", subsection "Configuration" and its configuration table, serves with
  * an FP8 key-value cache; section "Low-Precision Training" describes the
@@ -238,7 +259,8 @@ const char* rl_attn_last_error(void);
  * (device, stream) since the last check met an out-of-range page id, length
  * or indptr on the device (those values were clamped), an invalid FP8 scale,
  * or work beyond its workspace's capacity, RL_OK otherwise, and clears the
- * error word. Allocates nothing. */
+ * error word. Errors of rl_attn_decode_noalloc calls on this device are
+ * included, whatever their stream. Allocates nothing. */
 int rl_attn_check_device_errors(void* stream);
 
 /* Grows this (device, stream)'s workspace to at least `bytes` now, so later

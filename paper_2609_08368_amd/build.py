@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "librlattn.so")
 ARCH = os.environ.get("RL_ATTN_ARCH", "gfx950")
 
-SOURCES = ["decode.hip", "extend.hip", "append.hip", "diag.hip", "rl_attn_host.cpp"]
+SOURCES = ["decode.hip", "extend.hip", "append.hip", "diag.hip", "scratch.hip", "rl_attn_host.cpp"]
 
 
 def hipcc() -> str:

@@ -171,6 +171,16 @@ struct KernelTimer {
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream, KernelTimer* timer);
 
+// Statically allocated device scratch of the allocation-free decode entry point:
+// kScratchBytes per device; the first kScratchErrBytes hold its error word, the
+// rest its workspace. scratch_address() returns the current device's copy (its
+// address is looked up once per device, and the error word cleared then unless
+// `stream` is being captured); scratch_address_if_set_up() returns it only if
+// an earlier call already looked it up.
+constexpr size_t kScratchBytes = size_t(128) << 20;
+constexpr size_t kScratchErrBytes = 256;
+hipError_t scratch_address(hipStream_t stream, void** ptr);
+bool scratch_address_if_set_up(void** ptr);
 // Measurement aids (see rl_attn_diag.h): a grid-stride read of `bytes` and a
 // register-only bf16 MFMA loop.
 hipError_t launch_diag_read(const void* buf, size_t bytes, unsigned* sink, int cus, hipStream_t stream);

@@ -231,18 +231,33 @@ int acquire_ws(hipStream_t st, size_t need, Workspace** out) {
   return RL_OK;
 }
 
-// A call's workspace: this (device, stream)'s library workspace (grown with
-// hipMalloc) and its error word.
+// Where a call's workspace comes from: this (device, stream)'s library
+// workspace (grown with hipMalloc), or, for the allocation-free entry point, the
+// device's static scratch array (its first bytes are that array's error word).
 struct WsView {
   char* ptr;
   int* err;
 };
 
-int get_ws(hipStream_t st, size_t need, WsView* v) {
-  Workspace* w = nullptr;
-  RL_TRY(acquire_ws(st, need, &w));
-  v->ptr = static_cast<char*>(w->ptr);
-  v->err = w->err;
+int get_ws(hipStream_t st, size_t need, bool noalloc, WsView* v) {
+  if (!noalloc) {
+    Workspace* w = nullptr;
+    RL_TRY(acquire_ws(st, need, &w));
+    v->ptr = static_cast<char*>(w->ptr);
+    v->err = w->err;
+    return RL_OK;
+  }
+  const size_t room = rl::kScratchBytes - rl::kScratchErrBytes;
+  if (need > room)
+    return fail(RL_ERR_WORKSPACE,
+                "this call needs %zu bytes of workspace; the allocation-free entry point has %zu "
+                "(a smaller batch, or rl_attn_decode_ex, which allocates)",
+                need, room);
+  void* p = nullptr;
+  const hipError_t e = rl::scratch_address(st, &p);
+  if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+  v->ptr = static_cast<char*>(p) + rl::kScratchErrBytes;
+  v->err = static_cast<int*>(p);
   return RL_OK;
 }
 
@@ -511,11 +526,11 @@ size_t extend_ws_bytes(int64_t B, int64_t total_q, int64_t Hkv, int64_t R, int* 
 // Work-unit shape, workspace and launch of an extend call whose arguments
 // (pages, q, lengths, output) are already filled in. prof_kind: which timing
 // slot the attention kernel is counted under.
-int run_extend(rl::ExtendArgs& a, hipStream_t st, int prof_kind) {
+int run_extend(rl::ExtendArgs& a, hipStream_t st, int prof_kind, bool noalloc = false) {
   int max_items = 0;
   const size_t bytes = extend_ws_bytes(a.B, a.total_q, a.Hkv, a.R, &max_items);
   WsView w{};
-  RL_TRY(get_ws(st, bytes, &w));
+  RL_TRY(get_ws(st, bytes, noalloc, &w));
   char* base = w.ptr;
   const ExtendShape s = extend_shape(a.R);
   a.rows_head = s.rows_head;
@@ -526,7 +541,7 @@ int run_extend(rl::ExtendArgs& a, hipStream_t st, int prof_kind) {
   a.ws.items = reinterpret_cast<int4*>(base + 256);
   a.ws.err = w.err;
   rl::KernelTimer slot;
-  rl::KernelTimer* timer = prof_timer(&slot, st);
+  rl::KernelTimer* timer = noalloc ? nullptr : prof_timer(&slot, st);
   hipError_t e = rl::launch_extend(a, st, timer);
   prof_commit(prof_kind, timer);
   if (e != hipSuccess) return hip_fail(e, "extend kernel launch");
@@ -536,7 +551,7 @@ int run_extend(rl::ExtendArgs& a, hipStream_t st, int prof_kind) {
 int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages, int kv_dtype,
                 const rl_tensor* k_scale, const rl_tensor* v_scale, const rl_tensor* block_table,
                 const rl_tensor* seq_lens, float scale, rl_tensor* out, rl_tensor* lse_out, const rl_attn_opts* opts,
-                void* stream) {
+                void* stream, bool noalloc = false) {
   Opts o;
   RL_TRY(read_opts(opts, &o));
   RL_TRY(check_scale(scale));
@@ -605,7 +620,7 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
     e.lse_st = lse_out ? (multi ? lse_st : lse_out->strides[0]) : 0;
     e.lse_sh = lse_out ? lse_out->strides[multi ? 2 : 1] : 0;
     e.decode_rows = (int)n_tok;
-    return run_extend(e, st, 0);
+    return run_extend(e, st, 0, noalloc);
   }
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -614,7 +629,7 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   const DecodeLayout lay = decode_layout(B, Hq, Hkv, a.kv.max_pages, a.kv.page_size, o.split_tokens, cus,
                                          o.prefix_share == RL_PREFIX_AUTO, kv_dtype == RL_FP8_E4M3, (int)n_tok);
   WsView w{};
-  RL_TRY(get_ws(st, lay.total, &w));
+  RL_TRY(get_ws(st, lay.total, noalloc, &w));
   char* base = w.ptr;
   a.q = q->data;
   a.q_sb = q->strides[0];
@@ -658,7 +673,7 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   a.ws.part_lse = reinterpret_cast<float*>(base + lay.off_pl);
   a.ws.err = w.err;
   rl::KernelTimer slot;
-  rl::KernelTimer* timer = prof_timer(&slot, st);
+  rl::KernelTimer* timer = noalloc ? nullptr : prof_timer(&slot, st);
   e = rl::launch_decode(a, st, timer);
   prof_commit(0, timer);
   if (e != hipSuccess) return hip_fail(e, "decode kernel launch");
@@ -820,6 +835,13 @@ int rl_attn_decode_ex(const rl_tensor* q, const rl_tensor* k_pages, const rl_ten
                      opts, stream);
 }
 
+int rl_attn_decode_noalloc(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages,
+                           const rl_tensor* block_table, const rl_tensor* seq_lens, float scale, rl_tensor* out,
+                           rl_tensor* lse_out, const rl_attn_opts* opts, void* stream) {
+  return decode_impl(q, k_pages, v_pages, RL_BF16, nullptr, nullptr, block_table, seq_lens, scale, out, lse_out,
+                     opts, stream, true);
+}
+
 int rl_attn_decode_fp8(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v_pages,
                        const rl_tensor* k_scale, const rl_tensor* v_scale, const rl_tensor* block_table,
                        const rl_tensor* seq_lens, float scale, rl_tensor* out, rl_tensor* lse_out,
@@ -925,14 +947,17 @@ int rl_attn_check_device_errors(void* stream) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-  // the error word of this stream's workspace, if a call made one (none is
-  // created here)
-  int* words[1] = {nullptr};
+  // the error words to read: this stream's workspace (if a call made one) and
+  // the device's scratch array (if an allocation-free call set it up); none is
+  // created here
+  int* words[2] = {nullptr, nullptr};
   {
     std::lock_guard<std::mutex> lk(g_mu);
     auto it = g_ws.find({dev, st});
     if (it != g_ws.end()) words[0] = it->second.err;
   }
+  void* sp = nullptr;
+  if (rl::scratch_address_if_set_up(&sp)) words[1] = static_cast<int*>(sp);
   e = hipStreamSynchronize(st);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
   int word = 0;

@@ -63,6 +63,7 @@ def lib() -> ctypes.CDLL:
         L.rl_attn_extend.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, vp]
         L.rl_attn_decode_ex.argtypes = [P, P, P, P, P, ctypes.c_float, P, P, ctypes.POINTER(RlOpts), vp]
         L.rl_attn_extend_ex.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, P, ctypes.POINTER(RlOpts), vp]
+        L.rl_attn_decode_noalloc.argtypes = [P, P, P, P, P, ctypes.c_float, P, P, ctypes.POINTER(RlOpts), vp]
         L.rl_attn_decode_fp8.argtypes = [P, P, P, P, P, P, P, ctypes.c_float, P, P, ctypes.POINTER(RlOpts), vp]
         L.rl_attn_extend_fp8.argtypes = [P, P, P, P, P, P, P, P, ctypes.c_float, P, P, ctypes.POINTER(RlOpts), vp]
         L.rl_attn_append_kv.argtypes = [P, P, P, P, P, P, P, vp]
@@ -85,6 +86,7 @@ def lib() -> ctypes.CDLL:
         L.rl_attn_diag_decode_capacity.argtypes = [ctypes.c_int64] * 6 + [ctypes.c_int32] * 4 + [i64p]
         L.rl_attn_diag_extend_capacity.argtypes = [ctypes.c_int64] * 4 + [i64p]
         for name in ("rl_attn_decode", "rl_attn_extend", "rl_attn_decode_ex", "rl_attn_extend_ex",
+                     "rl_attn_decode_noalloc",
                      "rl_attn_decode_fp8", "rl_attn_extend_fp8", "rl_attn_append_kv", "rl_attn_append_kv_fp8",
                      "rl_attn_merge", "rl_attn_check_device_errors", "rl_attn_reserve_workspace",
                      "rl_attn_profile_enable", "rl_attn_profile_read", "rl_attn_diag_read_bandwidth",
@@ -168,6 +170,19 @@ def decode(q, k_pages, v_pages, block_table, seq_lens, scale, out=None, lse=None
     _check(lib().rl_attn_decode_ex(_ref(view(q)), _ref(view(k_pages)), _ref(view(v_pages)),
                                    _ref(view(block_table)), _ref(view(seq_lens)), ctypes.c_float(scale),
                                    _ref(view(out)), _ref(view(lse)), ctypes.byref(o), _stream(stream)))
+    return out
+
+
+def decode_noalloc(q, k_pages, v_pages, block_table, seq_lens, scale, out=None, lse=None, *, split_tokens=0,
+                   prefix_share=True, deterministic=False, stream=None):
+    """``rl_attn_decode_noalloc``: decode with the library's static scratch array as workspace
+    (``out`` must be given by a caller that cannot allocate)."""
+    if out is None:
+        out = torch.empty_like(q)
+    o = _opts(split_tokens, prefix_share, False, deterministic)
+    _check(lib().rl_attn_decode_noalloc(_ref(view(q)), _ref(view(k_pages)), _ref(view(v_pages)),
+                                        _ref(view(block_table)), _ref(view(seq_lens)), ctypes.c_float(scale),
+                                        _ref(view(out)), _ref(view(lse)), ctypes.byref(o), _stream(stream)))
     return out
 
 
