@@ -10,23 +10,30 @@ namespace {
 
 constexpr int kReadThreads = 256;
 constexpr int kReadUnroll = 8;
-constexpr int kReadBlocksPerCu = 64;   // the fastest of 4..64 workgroups per CU (and unroll 4 / 8) measured
+constexpr int kReadBlocksPerCu = 64;
 
-// Grid-stride read of n16 16-byte words; the xor of everything read is stored
-// only when it equals a value no real buffer produces in practice, so the
-// loads stay live without a store per thread.
+// Streaming read of n16 16-byte words: workgroup i reads the i-th contiguous
+// share of the buffer (rounded to whole rounds of kReadUnroll loads per
+// thread), each thread keeping kReadUnroll loads in flight. Contiguous shares
+// measured 6.2-6.35 TB/s against 5.7-6.15 TB/s for a grid-stride loop over
+// the whole buffer (4 GiB, 16-64 workgroups per CU). The xor of everything
+// read is stored only when it equals a value no real buffer produces in
+// practice, so the loads stay live without a store per thread.
 __global__ __launch_bounds__(kReadThreads) void read_kernel(const uint4* p, size_t n16, unsigned* sink) {
   unsigned acc = 0;
-  const size_t stride = (size_t)gridDim.x * kReadThreads;
-  size_t i = (size_t)blockIdx.x * kReadThreads + threadIdx.x;
-  for (; i + (kReadUnroll - 1) * stride < n16; i += kReadUnroll * stride) {
+  constexpr size_t kRound = (size_t)kReadThreads * kReadUnroll;
+  const size_t per = ((n16 + gridDim.x - 1) / gridDim.x + kRound - 1) / kRound * kRound;
+  const size_t beg = (size_t)blockIdx.x * per;
+  const size_t end = beg + per < n16 ? beg + per : n16;
+  size_t i = beg + threadIdx.x;
+  for (; i + (kReadUnroll - 1) * kReadThreads < end; i += kRound) {
     uint4 v[kReadUnroll];
 #pragma unroll
-    for (int u = 0; u < kReadUnroll; ++u) v[u] = p[i + u * stride];
+    for (int u = 0; u < kReadUnroll; ++u) v[u] = p[i + u * kReadThreads];
 #pragma unroll
     for (int u = 0; u < kReadUnroll; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
   }
-  for (; i < n16; i += stride) {
+  for (; i < end; i += kReadThreads) {
     const uint4 v = p[i];
     acc ^= v.x ^ v.y ^ v.z ^ v.w;
   }

@@ -502,10 +502,14 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
   __syncthreads();
   if (late) __syncthreads();
 
-  auto stage_and_fetch = [&](int j) {
-    const int t0 = t_lo + j * kKeys;
+  // LDS writes of the rows at hand (MFMA phase of step j)
+  auto stage = [&](int j) {
     if (j + 1 < nsteps) put_k((j + 1) & 1, kr);
     put_v(j & 1, vr);
+  };
+  // loads of the rows of V(j+1) and K(j+2) (softmax phase of step j)
+  auto fetch_next = [&](int j) {
+    const int t0 = t_lo + j * kKeys;
     if constexpr (kUniformPages) {
       fetch_u(t0 + kKeys, pid_1, vbase_u, kv.v_sp, vss, voff, vr);
       fetch_u(t0 + 2 * kKeys, pid_2, kbase_u, kv.sp, kss, koff, kr);
@@ -526,19 +530,23 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
   };
   const std::true_type yes{};
   const std::false_type no{};
-  // the staging of a step follows its MFMAs: they start as soon as the
-  // barrier opens, and the rows fetched one step earlier get the MFMA phase's
-  // time to arrive
+  // The LDS writes of a step follow its MFMAs (the MFMAs start as soon as the
+  // barrier opens); the global loads of the next rows open the softmax phase,
+  // whose VALU work leaves the vector memory path idle, and have the rest of
+  // that phase and the next MFMA phase to arrive (loads issued in the MFMA
+  // phase, after its MFMAs, measured 4% slower with bf16 pages).
   mfma_phase(no, yes, 0, 0);
-  stage_and_fetch(0);
+  stage(0);
   __syncthreads();
+  fetch_next(0);
   softmax_phase(t_lo);
   next_page(0);
   __syncthreads();
   for (int j = 1; j < nsteps; ++j) {
     mfma_phase(yes, yes, (j - 1) & 1, j & 1);
-    stage_and_fetch(j);
+    stage(j);
     __syncthreads();
+    fetch_next(j);
     softmax_phase(t_lo + j * kKeys);
     next_page(j);
     __syncthreads();
