@@ -164,7 +164,8 @@ def pmc_workload(kind: str = "ragged"):
     E4M3 pages; ragged-mtp4: the same pages with 4 query tokens per sequence;
     extend: two multi-turn extend calls; group / group-noshare: three decode calls
     of the 16x8 trajectory-group batch with prefix sharing on / off, then the same
-    calibration copies."""
+    calibration copies; branch / branch-noshare: the same for the 16x8 branching
+    batch (prompt, half-group and pair prefixes shared)."""
     import torch
 
     from paper_2609_08368_amd import rl_attn as ra
@@ -172,7 +173,8 @@ def pmc_workload(kind: str = "ragged"):
 
     dev = torch.device("cuda:0")
     w = {"ragged": wl.decode_ragged, "ragged-fp8": wl.decode_ragged, "ragged-mtp4": wl.decode_ragged,
-         "extend": wl.extend_multiturn}.get(kind, wl.decode_group_prefix)()
+         "extend": wl.extend_multiturn, "branch": wl.decode_branching,
+         "branch-noshare": wl.decode_branching}.get(kind, wl.decode_group_prefix)()
     fp8 = kind == "ragged-fp8"
     t = (wl.materialize_fp8 if fp8 else wl.materialize)(w, dev, poison=False)
     out = torch.empty_like(t["q"])
@@ -183,7 +185,7 @@ def pmc_workload(kind: str = "ragged"):
         torch.cuda.synchronize()
         print(json.dumps({"pmc_workload": kind, "flops": w.flops()}), flush=True)
         return
-    share = {"prefix_share": kind != "group-noshare"}
+    share = {"prefix_share": not kind.endswith("-noshare")}
     if kind == "ragged-mtp4":
         g = torch.Generator(device=dev)
         g.manual_seed(904)
@@ -209,7 +211,8 @@ def pmc_workload(kind: str = "ragged"):
 
 def prefix_study(steps: int = 20):
     """Group-prefix decode with prefix sharing on and off: the 16x8 group batch
-    (4096 shared tokens) and its long-prompt variant (32768 shared tokens)."""
+    (4096 shared tokens), its long-prompt variant (32768 shared tokens) and the
+    16x8 branching batch (4096 tokens per group, 2048 per half, 1024 per pair)."""
     import torch
 
     from paper_2609_08368_amd import rl_attn as ra
@@ -217,7 +220,7 @@ def prefix_study(steps: int = 20):
 
     dev = torch.device("cuda:0")
     res = {}
-    for w in (wl.decode_group_prefix(), wl.decode_group_long_prefix()):
+    for w in (wl.decode_group_prefix(), wl.decode_group_long_prefix(), wl.decode_branching()):
         t = wl.materialize(w, dev, poison=False)
         out = torch.empty_like(t["q"])
         row = {"unique_kv_bytes": w.kv_bytes(unique=True), "logical_kv_bytes": w.kv_bytes()}
@@ -554,7 +557,8 @@ def main():
                     help="scales the oracle baseline's wall-time budgets (15: 33 s over the five workloads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pmc-workload", nargs="?", const="ragged",
-                    choices=["ragged", "ragged-fp8", "ragged-mtp4", "extend", "group", "group-noshare"],
+                    choices=["ragged", "ragged-fp8", "ragged-mtp4", "extend", "group", "group-noshare", "branch",
+                             "branch-noshare"],
                     help="run only what a counter run profiles")
     ap.add_argument("--summarize-counters", metavar="PMC_DIR", help="per-kernel means of a rocprofv3 --pmc run")
     ap.add_argument("--prefix-study", action="store_true", help="time group-prefix decode with sharing on and off")

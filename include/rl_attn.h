@@ -167,10 +167,10 @@ int rl_attn_extend_ex(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_t
  * (code under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc). Arguments, results and options are those of rl_attn_decode_ex
  * (bf16 pages), and it runs the same kernels; its workspace is instead a
- * statically allocated array of 128 MiB per device (its first 256 bytes are an
+ * statically allocated array of 160 MiB per device (its first 256 bytes are an
  * error word), held by every device the library runs on until the process ends.
  * The call makes no hipMalloc, hipFree or other allocating call.
- * Limit: a call whose workspace would exceed 128 MiB - 256 B is rejected with
+ * Limit: a call whose workspace would exceed 160 MiB - 256 B is rejected with
  * RL_ERR_WORKSPACE before any launch (the workspace grows with the batch, the
  * query heads and query tokens per sequence, and, with a forced split, with
  * max_pages * page_size / split_tokens; e.g. batch 128 with 96 query heads, one

@@ -31,7 +31,7 @@ constexpr int kMinWorkerKeys = 256; // fewest keys per private-pass worker (auto
 constexpr int kTile = 32;          // keys per inner iteration of the private kernel
 constexpr int kGroupMax = 1024;    // batches up to this size get trajectory-group detection
 constexpr int kIntMax = 0x7fffffff;
-constexpr int kHashBits = 11;     // planner hash table: 2048 slots for up to kGroupMax first page ids
+constexpr int kHashBits = 11;     // planner hash table: 2048 slots for up to kGroupMax (parent, page) keys
 
 __device__ __forceinline__ int clamp_len(int L, int max_tokens, int* bad) {
   if (L < 0 || L > max_tokens) {
@@ -43,12 +43,24 @@ __device__ __forceinline__ int clamp_len(int L, int max_tokens, int* bad) {
 
 __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
-// Slot of first page ids in the planner's hash table (multiplicative hashing).
-__device__ __forceinline__ int page_hash(int key) { return (int)(((uint32_t)key * 2654435761u) >> (32 - kHashBits)); }
+// Key of the planner's hash table: (parent node leader + 1, page id); ~0 = empty.
+__device__ __forceinline__ unsigned long long node_key(int parent, int page) {
+  return ((unsigned long long)(uint32_t)(parent + 1) << 32) | (uint32_t)page;
+}
+__device__ __forceinline__ int key_hash(unsigned long long key) {
+  return (int)((((uint32_t)key ^ (uint32_t)(key >> 32) * 0x9e3779b1u) * 2654435761u) >> (32 - kHashBits));
+}
 
 __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
-  __shared__ int sL[kGroupMax], sLead[kGroupMax], sKmin[kGroupMax], sCnt[kGroupMax], sSg[kGroupMax];
-  __shared__ int hKey[1 << kHashBits], hMin[1 << kHashBits];
+  // per sequence (small batches): length; per level: the leader of its shared
+  // node (-1: none) and the end of its shared keys after that level; per node
+  // (indexed by its leader): members and first sub-group
+  __shared__ int sL[kGroupMax];
+  __shared__ int sLead[kPrefixLevels][kGroupMax], sEnd[kPrefixLevels][kGroupMax];
+  __shared__ int sNum[kPrefixLevels][kGroupMax], sSg[kPrefixLevels][kGroupMax];
+  __shared__ int sKmin[kGroupMax], sCnt[kGroupMax];
+  __shared__ unsigned long long hKey[1 << kHashBits];
+  __shared__ int hMin[1 << kHashBits];
   __shared__ int wave_tot[16];
   __shared__ long long wsum[16];
   const int tid = threadIdx.x, nthr = blockDim.x, lane = tid & 63, wave = tid >> 6, nwaves = nthr >> 6;
@@ -61,22 +73,12 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
   const uint32_t bt_sj = (uint32_t)a.kv.bt_sj;
   int bad = 0, cap_bad = 0;
 
-  if (grouping)
-    for (int i = tid; i < (1 << kHashBits); i += nthr) {
-      hKey[i] = -1;
-      hMin[i] = kIntMax;
-    }
   // lengths and their sum
   long long sum = 0;
   for (int b = tid; b < a.B; b += nthr) {
     const int L = clamp_len(a.lens[b * a.lens_s], max_tokens, &bad);
     sum += L;
-    if (small) {
-      sL[b] = L;
-      sKmin[b] = kIntMax;
-      sCnt[b] = 0;
-      sLead[b] = b;
-    }
+    if (small) sL[b] = L;
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
@@ -92,89 +94,147 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
     C = (int)(per < kMinSplit ? kMinSplit : per);
   }
 
+  // Shared prefix pages as a tree of nodes, level by level. At level 0 the
+  // sequences whose block tables start with the same page id form a node (the
+  // trajectory group: G attempts at one prompt share its cached prefix); at
+  // level v > 0 the members of a level v-1 node are split by the page id that
+  // follows the node's shared range (sessions that branch after a common turn).
+  // A node's leader is its lowest-indexed member; the node shares the leading
+  // full pages that every member has in common with the leader (from the
+  // parent's end on), and is kept if it has another member and at least one
+  // such page. Its keys [parent end, node end) are then read once for all its
+  // members by the group-prefix pass.
   if (grouping) {
-    // leader = lowest-indexed sequence with the same first page id, found
-    // through an LDS hash table keyed by that id (open addressing)
-    const int b = tid;
-    const int key = (b < a.B && (sL[b] >> lg) > 0) ? a.kv.bt[(int64_t)b * a.kv.bt_sb] : -1;
-    if (key >= 0) {
-      int h = page_hash(key);
-      for (;;) {
-        const int prev = atomicCAS(&hKey[h], -1, key);
-        if (prev == -1 || prev == key) {
-          atomicMin(&hMin[h], b);
-          break;
-        }
-        h = (h + 1) & ((1 << kHashBits) - 1);
+    for (int v = 0; v < kPrefixLevels; ++v) {
+      for (int i = tid; i < (1 << kHashBits); i += nthr) {
+        hKey[i] = ~0ull;
+        hMin[i] = kIntMax;
       }
-    }
-    __syncthreads();
-    if (key >= 0) {
-      int h = page_hash(key);
-      while (hKey[h] != key) h = (h + 1) & ((1 << kHashBits) - 1);
-      sLead[b] = hMin[h];
-    }
-    __syncthreads();
-    // leading full pages each member shares with its leader (one wave per
-    // member, 64 pages per comparison); the group shares the minimum
-    for (int m = wave; m < a.B; m += nwaves) {
-      const int lead = sLead[m];
-      if (lead == m) continue;
-      const int lim = min(sL[m], sL[lead]) >> lg;
-      const int* rb = a.kv.bt + (int64_t)m * a.kv.bt_sb;
-      const int* rl = a.kv.bt + (int64_t)lead * a.kv.bt_sb;
-      int k = lim;
-      for (int c = 0; c < lim; c += 64) {
-        const int kk = c + lane;
-        const bool differ = kk < lim && rb[__umul24((uint32_t)kk, bt_sj)] != rl[__umul24((uint32_t)kk, bt_sj)];
-        const unsigned long long mask = __builtin_amdgcn_ballot_w64(differ);
-        if (mask) {
-          k = c + __builtin_ctzll(mask);
-          break;
+      for (int i = tid; i < a.B; i += nthr) {
+        sKmin[i] = kIntMax;
+        sCnt[i] = 0;
+      }
+      __syncthreads();
+      const int b = tid;
+      const int parent = (b < a.B && v > 0) ? sLead[v - 1][b] : -1;
+      const int start = (b < a.B && v > 0) ? sEnd[v - 1][b] : 0;
+      // takes part: in a node at the previous level (or at level 0), with a
+      // full page at the position that follows the shared range
+      const bool part = b < a.B && (v == 0 || parent >= 0) && (sL[b] >> lg) > (start >> lg);
+      const int page = part ? a.kv.bt[(int64_t)b * a.kv.bt_sb + (int64_t)__umul24((uint32_t)(start >> lg), bt_sj)] : 0;
+      const unsigned long long key = node_key(parent, page);
+      if (part) {
+        int h = key_hash(key);
+        for (;;) {
+          const unsigned long long prev = atomicCAS(&hKey[h], ~0ull, key);
+          if (prev == ~0ull || prev == key) {
+            atomicMin(&hMin[h], b);
+            break;
+          }
+          h = (h + 1) & ((1 << kHashBits) - 1);
         }
       }
-      if (lane == 0) {
-        atomicMin(&sKmin[lead], k);
-        atomicAdd(&sCnt[lead], 1);
+      __syncthreads();
+      if (b < a.B) {
+        int lead = -1;
+        if (part) {
+          int h = key_hash(key);
+          while (hKey[h] != key) h = (h + 1) & ((1 << kHashBits) - 1);
+          lead = hMin[h];
+        }
+        sLead[v][b] = lead;
       }
+      __syncthreads();
+      // leading full pages each member shares with its leader from the parent's
+      // end on (one wave per member, 64 pages per comparison); the node shares
+      // the minimum
+      for (int m = wave; m < a.B; m += nwaves) {
+        const int lead = sLead[v][m];
+        if (lead < 0 || lead == m) continue;
+        const int p0 = (v == 0 ? 0 : sEnd[v - 1][m]) >> lg;
+        const int lim = min(sL[m], sL[lead]) >> lg;
+        const int* rb = a.kv.bt + (int64_t)m * a.kv.bt_sb;
+        const int* rl = a.kv.bt + (int64_t)lead * a.kv.bt_sb;
+        int k = lim;
+        for (int c = p0; c < lim; c += 64) {
+          const int kk = c + lane;
+          const bool differ = kk < lim && rb[__umul24((uint32_t)kk, bt_sj)] != rl[__umul24((uint32_t)kk, bt_sj)];
+          const unsigned long long mask = __builtin_amdgcn_ballot_w64(differ);
+          if (mask) {
+            k = c + __builtin_ctzll(mask);
+            break;
+          }
+        }
+        if (lane == 0) {
+          atomicMin(&sKmin[lead], k);
+          atomicAdd(&sCnt[lead], 1);
+        }
+      }
+      __syncthreads();
+      if (b < a.B) {
+        const int lead = sLead[v][b];
+        const bool kept = lead >= 0 && sCnt[lead] >= 1 && sKmin[lead] > (start >> lg);
+        sLead[v][b] = kept ? lead : -1;
+        sEnd[v][b] = kept ? sKmin[lead] * P : start;
+        sNum[v][b] = (kept && lead == b) ? sCnt[b] + 1 : 0;
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
-  // a sequence shares with its group when the group has another member and at least one full page
-  auto shared_keys = [&](int b) -> int {
-    if (!grouping) return 0;
-    const int lead = sLead[b];
-    return (sCnt[lead] >= 1 && sKmin[lead] >= 1) ? sKmin[lead] * P : 0;
+  // keys [*t0, *t1) of sequence b shared at level v, if b is in a node there
+  auto level_range = [&](int v, int b, int* t0, int* t1) -> bool {
+    *t0 = v == 0 ? 0 : sEnd[v - 1][b];
+    *t1 = sEnd[v][b];
+    return sLead[v][b] >= 0;
   };
+  // all shared keys of sequence b: its private keys start there
+  auto shared_keys = [&](int b) -> int { return grouping ? sEnd[kPrefixLevels - 1][b] : 0; };
   const int cap = a.group_cap;
 
-  // sub-groups of at most `cap` members: bases by an exclusive scan over leaders
+  // sub-groups of at most `cap` members: bases by exclusive scans over the
+  // nodes' leaders, level after level
   int n_sg = 0;
   if (grouping) {
-    const int b = tid;
-    int nsub = 0;
-    if (b < a.B && sLead[b] == b && shared_keys(b) > 0) nsub = ceil_div(sCnt[b] + 1, cap);
-    const int excl = block_exclusive_scan(nsub, &n_sg, wave_tot);
-    if (b < a.B) sSg[b] = excl;
+    long long tot_sh = 0;
+    for (int v = 0; v < kPrefixLevels; ++v) {
+      const int b = tid;
+      int nsub = 0, t0 = 0, t1 = 0;
+      if (b < a.B && level_range(v, b, &t0, &t1) && sLead[v][b] == b) nsub = ceil_div(sNum[v][b], cap);
+      int tot;
+      const int excl = block_exclusive_scan(nsub, &tot, wave_tot);
+      if (b < a.B) sSg[v][b] = n_sg + excl;
+      n_sg += tot;
+      long long tsh;
+      (void)block_exclusive_scan64(nsub > 0 ? (long long)nsub * (t1 - t0) : 0, &tsh, wsum);
+      tot_sh += tsh;
+    }
     // Split of the shared keys: at least C, and large enough that the shared
     // items of all sub-groups times the KV heads fit the group-prefix grid in
     // one round (its workgroups are all resident; a second, partly filled
     // round would double the pass's time)
-    long long tot_sh;
-    (void)block_exclusive_scan64(nsub > 0 ? (long long)nsub * shared_keys(b) : 0, &tot_sh, wsum);
     if (a.forced_split <= 0 && tot_sh > 0) {
       long long per = (tot_sh * a.Hkv + a.prefix_grid - 1) / a.prefix_grid;
       per = (per + 63) & ~63LL;
       if (per > C) C = (int)per;
     }
   }
+  // shared splits of sequence b over all levels
+  auto shared_splits = [&](int b) -> int {
+    int n = 0;
+    if (grouping)
+      for (int v = 0; v < kPrefixLevels; ++v) {
+        int t0, t1;
+        if (level_range(v, b, &t0, &t1)) n += ceil_div(t1 - t0, C);
+      }
+    return n;
+  };
 
   // Private keys, counted in tiles of kTile keys (each sequence's range is
   // rounded up to whole tiles, so every piece starts on a tile boundary):
   // prefix sums per sequence, then the number of workers (a worker takes W / n
   // tiles, at least kMinWorkerKeys keys or the forced split, and at most
   // max_workers of them run)
-  __syncthreads();   // the sum's per-wave totals are read before they are reused
+  __syncthreads();   // the sums' per-wave totals are read before they are reused
   long long poff = 0;
   for (int b0 = 0; b0 < a.B; b0 += nthr) {
     const int b = b0 + tid;
@@ -201,8 +261,9 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
   // workers whose share starts before tile y of the concatenation (0 < y <= W)
   auto starts_before = [&](long long y) -> long long { return (y * nwork + W - 1) / W; };
 
-  // Per sequence: its shared splits, then one private piece per worker share
-  // it overlaps (a worker start strictly inside the range begins a new piece)
+  // Per sequence: its shared splits (level by level), then one private piece
+  // per worker share it overlaps (a worker start strictly inside the range
+  // begins a new piece)
   int slot_off = 0;
   for (int b0 = 0; b0 < a.B; b0 += nthr) {
     const int b = b0 + tid;
@@ -212,7 +273,7 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
       int dummy = 0;
       L = small ? sL[b] : clamp_len(a.lens[b * a.lens_s], max_tokens, &dummy);
       S = shared_keys(b);
-      nsh = S > 0 ? ceil_div(S, C) : 0;
+      nsh = shared_splits(b);
       const long long p0 = a.ws.pref[b], p1 = a.ws.pref[b + 1];
       npriv = p1 > p0 ? (int)(1 + starts_before(p1) - starts_before(p0 + 1)) : 0;
       empty = L == 0;
@@ -229,14 +290,23 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
       a.ws.nparts[b] = empty ? -1 : (fits ? nslots : -2);
       a.ws.base[b] = slot_base;
       a.ws.seqs[b] = make_int4(S, !fits ? kSlotDropped : (direct ? kSlotDirect : slot_base + nsh), L, fits ? 1 : 0);
-      if (S > 0) {
-        const int lead = sLead[b];
+      // its place in the sub-groups of every node it belongs to; a node's
+      // splits take the member's slots after those of its ancestors
+      int off = 0;
+      for (int v = 0; v < kPrefixLevels && S > 0; ++v) {
+        int t0, t1;
+        if (!level_range(v, b, &t0, &t1)) continue;
+        const int lead = sLead[v][b];
         int rank = 0;
-        if (b != lead)
-          for (int j = lead + 1; j <= b; ++j) rank += sLead[j] == lead;
-        const int sg = sSg[lead] + rank / cap, pos = rank % cap;
+        for (int j = lead + 1; j <= b; ++j) rank += sLead[v][j] == lead;
+        const int sg = sSg[v][lead] + rank / cap, pos = rank % cap;
+        const int n_split = ceil_div(t1 - t0, C);
         a.ws.sg_members[sg * cap + pos] = b;
-        if (pos == 0) a.ws.sgroups[sg] = make_int4(b, min(cap, sCnt[lead] + 1 - (rank / cap) * cap), S, nsh);
+        if (pos == 0) {
+          a.ws.sgroups[sg] = make_int4(b, min(cap, sNum[v][lead] - (rank / cap) * cap), t1, n_split);
+          a.ws.sg_range[sg] = make_int2(t0, off);
+        }
+        off += n_split;
       }
     }
     slot_off += slot_tot;
@@ -248,13 +318,17 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
   for (int g0 = 0; g0 < n_sg; g0 += nthr) {
     const int sg = g0 + tid;
     int4 info = make_int4(0, 0, 0, 0);
-    if (sg < n_sg) info = a.ws.sgroups[sg];
+    int2 rng = make_int2(0, 0);
+    if (sg < n_sg) {
+      info = a.ws.sgroups[sg];
+      rng = a.ws.sg_range[sg];
+    }
     int tot;
     const int base = sitem_off + block_exclusive_scan(sg < n_sg ? info.w : 0, &tot, wave_tot);
     if (sg < n_sg)
       for (int s = 0; s < info.w; ++s) {
         if (base + s < a.max_items)
-          a.ws.sitems[base + s] = make_int4(sg, s * C, min(info.z, (s + 1) * C), s);
+          a.ws.sitems[base + s] = make_int4(sg, rng.x + s * C, min(info.z, rng.x + (s + 1) * C), rng.y + s);
         else
           cap_bad = 1;
       }
@@ -738,11 +812,11 @@ __global__ __launch_bounds__(kMultiWaves * 64, 2) void decode_multi_kernel(Decod
   if (bad_scale) atomicOr(a.ws.err, kErrScale);
 }
 
-// Group-prefix pass: one workgroup per (shared item, KV head) computes the
-// shared keys of a sub-group once for all its members' query rows (row r ->
-// member r / (n R), then query token, then query head), reading each shared
-// page once, and writes one partial per member into that member's slot for
-// this split.
+// Group-prefix pass: one workgroup per (shared item, KV head) computes a split
+// of a node's shared keys once for all the query rows of one of its sub-groups
+// (row r -> member r / (n R), then query token, then query head), reading each
+// shared page once per sub-group, and writes one partial per member into that
+// member's slot for this split.
 constexpr int kPrefixWaves = 4;         // waves per group-prefix workgroup: 128 member rows
 
 template <bool kFp8>
@@ -755,7 +829,7 @@ __global__ __launch_bounds__(kPrefixWaves * 64, 2) void prefix_kernel(DecodeArgs
     const int item = wi / a.Hkv;
     const int g = wi - item * a.Hkv;
     const int4 it = a.ws.sitems[item];
-    const int sg = it.x, t0 = it.y, t1 = it.z, split = it.w;
+    const int sg = it.x, t0 = it.y, t1 = it.z, split = it.w;   // split: slot offset in each member's slots
     const int4 info = a.ws.sgroups[sg];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = wave * kWaveRows + (lane & 31);
@@ -780,9 +854,11 @@ __global__ __launch_bounds__(kPrefixWaves * 64, 2) void prefix_kernel(DecodeArgs
     float m_run = kNegInf, l_run = 0.f;
     int bad = 0, bad_scale = 0;
     const KvScales dq = kv_scales<kFp8>(a.kv, g, &bad_scale);
-    tile_attend<kPrefixWaves, kFp8>(a.kv, a.scale * dq.k, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g, t0, t1,
-                                           a.n_tok == 1 ? t1 : t0, limit, qv, lds, o, m_run, l_run, bad, -1,
-                                           wave * kWaveRows / rows_m < info.y);
+    // a node below the first level starts where its parent ends, a page
+    // boundary that need not be a step boundary: keys below t0 are masked
+    tile_attend<kPrefixWaves, kFp8>(a.kv, a.scale * dq.k, a.kv.bt + (int64_t)info.x * a.kv.bt_sb, g,
+                                           t0 & ~(kKeys - 1), t1, a.n_tok == 1 ? t1 : t0, limit, qv, lds, o, m_run,
+                                           l_run, bad, t0, wave * kWaveRows / rows_m < info.y);
     const HeadResult res = finish(m_run, sum_l32(l_run));
     if (row_ok) {
       const int slot = a.ws.base[b] + split;

@@ -38,12 +38,18 @@ struct PagedKV {
   int64_t ks_s, vs_s;
 };
 
+// Levels of nested shared prefix pages the decode planner detects: the prefix a
+// trajectory group shares, then prefixes shared by subsets of it (sessions
+// that branch after a common turn).
+constexpr int kPrefixLevels = 3;
+
 // Workspace carve-up of one decode call. Private keys: sequence b owns
 // [pref[b], pref[b+1]) of the concatenation of all sequences' private key
 // ranges (its keys S_b .. L_b - 1), and worker w of n takes the equal share
 // [w W / n, (w+1) W / n) of it, cut at sequence boundaries into pieces.
-// Shared items cover the prefix pages a trajectory group shares and serve
-// every member of one sub-group (at most 128 query rows). Partial results
+// Shared items cover the prefix pages a node of trajectory-group members
+// shares (see the planner) and serve every member of one sub-group (at most
+// 128 query rows). Partial results
 // live in "slots"; sequence b owns slots base[b] .. base[b] + nparts[b] - 1:
 // its shared splits, then its private pieces in key order (nparts[b] == 0:
 // one piece, written directly; -1: an empty sequence, written by the combine;
@@ -56,9 +62,10 @@ struct DecodePlanWs {
   long long* pref; // [B + 1] prefix sums of private keys
   int4* seqs;      // [B] (shared keys S, slot of the first private piece, kSlotDirect or kSlotDropped, L,
                    //      1 if the sequence's slots fit the workspace)
-  int4* sitems;    // [max_items] (sub-group, first key, end key, split index)
-  int4* sgroups;   // [B] (sequence whose block table is read, members, shared keys, shared splits)
-  int* sg_members; // [B * group_cap] member sequences of each sub-group
+  int4* sitems;    // [max_items] (sub-group, first key, end key, slot offset in each member's slots)
+  int4* sgroups;   // [kPrefixLevels * B] (sequence whose block table is read, members, end key, splits)
+  int2* sg_range;  // [kPrefixLevels * B] (first key, slot offset of the first split)
+  int* sg_members; // [kPrefixLevels * B * group_cap] member sequences of each sub-group
   float* part_o;   // [max_slots, Hq, 128]
   float* part_lse; // [max_slots, Hq]
   int* err;        // device error word (persistent)
@@ -177,7 +184,7 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream, KernelTimer* t
 // address is looked up once per device, and the error word cleared then unless
 // `stream` is being captured); scratch_address_if_set_up() returns it only if
 // an earlier call already looked it up.
-constexpr size_t kScratchBytes = size_t(128) << 20;
+constexpr size_t kScratchBytes = size_t(160) << 20;
 constexpr size_t kScratchErrBytes = 256;
 hipError_t scratch_address(hipStream_t stream, void** ptr);
 bool scratch_address_if_set_up(void** ptr);

@@ -300,16 +300,18 @@ void prof_commit(int kind, rl::KernelTimer* t) {
 // ------------------------------------------------------------------- decode
 constexpr int64_t kMinSplitKeys = 256;   // the planner's smallest automatic split of shared keys
 
-// Capacities (see the planner): with split size C and T = sum(L) / C,
-// Private pieces <= workers + B, shared items <= T + B, partial slots <=
-// workers + T + 2B. An automatic shared split C keeps T at or below the target
+// Capacities (see the planner): with split size C, T = sum(L) / C and D =
+// kPrefixLevels (a member's shared keys are cut at most D times by node
+// boundaries), private pieces <= workers + B, shared items <= T + D B, partial
+// slots <= workers + T + (D + 1) B. An automatic shared split C keeps T at or below the target
 // item count, and C >= kMinSplitKeys keeps it at or below
 // B * ceil(max_pages * P / kMinSplitKeys); a forced C bounds T by
 // B * ceil(max_pages * P / C) and lets the private pass use up to that many
 // workers of C keys.
 struct DecodeLayout {
   int max_items, max_slots, max_workers, group_cap;
-  size_t off_nparts, off_base, off_pref, off_seqs, off_sitems, off_sgroups, off_members, off_po, off_pl, total;
+  size_t off_nparts, off_base, off_pref, off_seqs, off_sitems, off_sgroups, off_range, off_members, off_po, off_pl,
+      total;
 };
 
 int64_t decode_wgs_per_item(int64_t Hq, int64_t Hkv) {
@@ -362,9 +364,10 @@ DecodeLayout decode_layout_with(int64_t B, int64_t Hq, int64_t Hkv, int64_t max_
                                                   B * std::max<int64_t>(1, (max_tokens + kMinSplitKeys - 1) /
                                                                                kMinSplitKeys));
   const int64_t workers = split > 0 ? T : (int64_t)cus * wpc;
-  L.max_items = (int)std::min<int64_t>(T + B, INT32_MAX / 2);
+  const int64_t D = rl::kPrefixLevels;
+  L.max_items = (int)std::min<int64_t>(T + D * B, INT32_MAX / 2);
   L.max_workers = (int)std::min<int64_t>(std::max<int64_t>(1, workers), INT32_MAX / 64);
-  L.max_slots = (int)std::min<int64_t>(L.max_workers + T + 2 * B, INT32_MAX / 2);
+  L.max_slots = (int)std::min<int64_t>(L.max_workers + T + (D + 1) * B, INT32_MAX / 2);
   L.group_cap = (prefix_share && rows_kv <= 64) ? (int)(128 / rows_kv) : 0;
   size_t off = 256;  // header
   L.off_nparts = off;
@@ -378,9 +381,11 @@ DecodeLayout decode_layout_with(int64_t B, int64_t Hq, int64_t Hkv, int64_t max_
   L.off_sitems = off;
   off += align256((size_t)L.max_items * 16);
   L.off_sgroups = off;
-  off += align256((size_t)B * 16);
+  off += align256((size_t)D * B * 16);
+  L.off_range = off;
+  off += align256((size_t)D * B * 8);
   L.off_members = off;
-  off += align256((size_t)B * std::max(1, L.group_cap) * 4);
+  off += align256((size_t)D * B * std::max(1, L.group_cap) * 4);
   L.off_po = off;
   off += align256((size_t)L.max_slots * Hv * 128 * 4);
   L.off_pl = off;
@@ -668,6 +673,7 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   a.ws.seqs = reinterpret_cast<int4*>(base + lay.off_seqs);
   a.ws.sitems = reinterpret_cast<int4*>(base + lay.off_sitems);
   a.ws.sgroups = reinterpret_cast<int4*>(base + lay.off_sgroups);
+  a.ws.sg_range = reinterpret_cast<int2*>(base + lay.off_range);
   a.ws.sg_members = reinterpret_cast<int*>(base + lay.off_members);
   a.ws.part_o = reinterpret_cast<float*>(base + lay.off_po);
   a.ws.part_lse = reinterpret_cast<float*>(base + lay.off_pl);

@@ -121,6 +121,48 @@ def _assign_pages(rng, lens, page_size, pool_pages=None, group_size=1, shared_to
     return table, pool, poison
 
 
+def _assign_tree_pages(rng, lens, page_size, levels):
+    """Pages for branching sessions: ``levels`` = [(block size, tokens), ...] with
+    each block size dividing the one before. Consecutive members in blocks of the
+    level-k size reference the same physical pages for that level's tokens,
+    which follow the previous levels' tokens (all token counts multiples of the
+    page size); the rest of each sequence has pages of its own. Page ids are a
+    seeded permutation of the pool. Returns (block_table, num_pages, poison_page).
+    """
+    b_count = len(lens)
+    used = [-(-int(l) // page_size) for l in lens]
+    bounds, t = [], 0
+    for size, tokens in levels:
+        if tokens % page_size:
+            raise ValueError("level tokens must be whole pages")
+        bounds.append((size, t // page_size, (t + tokens) // page_size))
+        t += tokens
+    need = 0
+    for b in range(b_count):
+        for size, p0, p1 in bounds:
+            if b % size == 0:
+                need += max(0, min(used[b], p1) - p0)
+        need += max(0, used[b] - bounds[-1][2])
+    pool = need + 1
+    perm = rng.permutation(pool).astype(np.int32)
+    poison = int(perm[need])
+    table = np.full((b_count, max(1, max(used))), poison, dtype=np.int32)
+    nxt = 0
+    for b in range(b_count):
+        for size, p0, p1 in bounds:
+            first = b - b % size
+            for j in range(p0, min(used[b], p1)):
+                if b == first:
+                    table[b, j] = perm[nxt]
+                    nxt += 1
+                else:
+                    table[b, j] = table[first, j]
+        for j in range(bounds[-1][2], used[b]):
+            table[b, j] = perm[nxt]
+            nxt += 1
+    return table, pool, poison
+
+
 def decode_tiny(seed: int = 1001) -> Paged:
     """Batch 4, 8 query / 2 KV heads, contexts 128/256/384/512, page 16, pool of 256 pages."""
     rng = np.random.default_rng(seed)
@@ -195,16 +237,40 @@ def decode_group_long_prefix(seed: int = 1006) -> Paged:
                  table, lens, np.ones(128, np.int32), poison, shared_prefix_pages=shared // 64, group_size=8)
 
 
+def decode_branching(seed: int = 1007, shuffle: bool = False) -> Paged:
+    """Branching sessions: 16 prompts x G=8 trajectories sharing a 4096-token prompt;
+    each group branches into 2 subsets of 4 sharing the next 2048 tokens (a common
+    turn), each of those into pairs sharing 1024 more; then private continuations
+    U{512..4096}. 64 query / 8 KV heads, page 64. ``shuffle`` permutes the batch."""
+    rng = np.random.default_rng(seed)
+    levels = [(8, 4096), (4, 2048), (2, 1024)]
+    priv = rng.integers(512, 4096, size=128, endpoint=True)
+    lens = (4096 + 2048 + 1024 + priv).astype(np.int32)
+    table, pool, poison = _assign_tree_pages(rng, lens, 64, levels)
+    if shuffle:
+        order = rng.permutation(len(lens))
+        lens, table = lens[order], table[order]
+    return Paged("decode_branching_16x8_tree4096-2048-1024_h64kv8_p64", "decode", seed, 64, 8, 64, pool,
+                 table, lens, np.ones(len(lens), np.int32), poison, shared_prefix_pages=64, group_size=8)
+
+
 def custom(seed: int, kind: str, kv_lens, q_lens=None, hq: int = 8, hkv: int = 2, page_size: int = 16,
-           pool_extra: int = 3, group_size: int = 1, shared_tokens: int = 0, kv_head_scale=None) -> Paged:
-    """A small workload of any shape (tests)."""
+           pool_extra: int = 3, group_size: int = 1, shared_tokens: int = 0, kv_head_scale=None,
+           branches=None) -> Paged:
+    """A small workload of any shape (tests). ``branches``: [(block size, tokens), ...]
+    gives tree-shaped sharing (see _assign_tree_pages) instead of ``group_size`` /
+    ``shared_tokens``."""
     rng = np.random.default_rng(seed)
     lens = np.asarray(kv_lens, dtype=np.int32)
     ql = np.ones(len(lens), np.int32) if q_lens is None else np.asarray(q_lens, dtype=np.int32)
     used = [-(-int(l) // page_size) for l in lens]
     need = sum(used) + 1
-    table, pool, poison = _assign_pages(rng, lens, page_size, pool_pages=need + pool_extra,
-                                        group_size=group_size, shared_tokens=shared_tokens)
+    if branches:
+        table, pool, poison = _assign_tree_pages(rng, lens, page_size, branches)
+        group_size, shared_tokens = branches[0]
+    else:
+        table, pool, poison = _assign_pages(rng, lens, page_size, pool_pages=need + pool_extra,
+                                            group_size=group_size, shared_tokens=shared_tokens)
     scales = None if kv_head_scale is None else np.asarray(kv_head_scale, np.float32)
     return Paged(f"custom_{kind}_{seed}", kind, seed, hq, hkv, page_size, pool, table, lens, ql, poison,
                  kv_head_scale=scales, shared_prefix_pages=shared_tokens // page_size, group_size=group_size)

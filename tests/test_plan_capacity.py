@@ -5,10 +5,12 @@ partial-result slots into a workspace whose capacities the host fixes before
 the launch, from sizes alone. A planner that needs more reports
 kErrCapacity instead of racing or dropping work, but that must never happen for
 a valid call. This test models the planners' counts in plain Python (split
-size, trajectory groups and sub-groups, shared items, equal-work worker shares
-and the pieces they cut, partial slots, extend work units), evaluates them on
-drawn batches (ragged and uniform lengths, empty sequences, trajectory groups
-with shared prefixes, forced splits, 1-64 query tokens, batches up to 3,000),
+size, the nodes of nested shared prefix ranges and their sub-groups, shared
+items, equal-work worker shares and the pieces they cut, partial slots, extend
+work units), evaluates them on drawn batches (ragged and uniform lengths, empty
+sequences, trajectory groups with shared prefixes, branching sessions with up
+to three nested shared ranges, forced splits, 1-64 query tokens, batches up to
+3,000),
 and checks each count against the capacities the library's host code computes
 (rl_attn_diag_decode_capacity / rl_attn_diag_extend_capacity).
 """
@@ -19,6 +21,7 @@ import numpy as np
 import pytest
 
 from paper_2609_08368_amd import rl_attn as ra
+from paper_2609_08368_amd import workloads as wl
 
 TILE = 32            # keys per private-pass tile
 MIN_SPLIT = 256      # smallest automatic split of shared keys
@@ -30,8 +33,11 @@ def ceil_div(a, b):
     return -(-a // b)
 
 
+LEVELS = 3          # nested levels of shared prefix pages the planner detects
+
+
 def plan_decode(lens, table, P, caps, forced_split):
-    """Counts the decode planner produces: (shared items, partial slots)."""
+    """Counts the decode planner produces: (shared items, partial slots, workers)."""
     B = len(lens)
     total = int(sum(lens))
     if forced_split > 0:
@@ -42,45 +48,61 @@ def plan_decode(lens, table, P, caps, forced_split):
         C = max(per, MIN_SPLIT)
     cap = caps["group_cap"]
     grouping = cap >= 2 and B <= GROUP_MAX
-    shared = [0] * B
-    subgroups = []       # (leader, members in the sub-group, shared keys)
+    lead = [[-1] * B for _ in range(LEVELS)]
+    end = [[0] * B for _ in range(LEVELS)]
+    num = [[0] * B for _ in range(LEVELS)]
     if grouping:
-        lead = list(range(B))
-        first = {}
-        for b in range(B):
-            if lens[b] // P > 0:
-                key = int(table[b][0])
-                first.setdefault(key, b)
-                lead[b] = first[key]
-        kmin = {b: None for b in range(B)}
-        cnt = [0] * B
-        for m in range(B):
-            l = lead[m]
-            if l == m:
-                continue
-            lim = min(lens[m], lens[l]) // P
-            k = lim
-            for j in range(lim):
-                if table[m][j] != table[l][j]:
-                    k = j
-                    break
-            kmin[l] = k if kmin[l] is None else min(kmin[l], k)
-            cnt[l] += 1
-        for b in range(B):
-            l = lead[b]
-            if cnt[l] >= 1 and kmin[l] is not None and kmin[l] >= 1:
-                shared[b] = kmin[l] * P
+        for v in range(LEVELS):
+            leads, first = [-1] * B, {}
+            for b in range(B):
+                parent = lead[v - 1][b] if v else -1
+                start = end[v - 1][b] if v else 0
+                if (v == 0 or parent >= 0) and lens[b] // P > start // P:
+                    key = (parent, int(table[b][start // P]))
+                    first.setdefault(key, b)
+                    leads[b] = first[key]
+            kmin, cnt = {}, [0] * B
+            for m in range(B):
+                l = leads[m]
+                if l < 0 or l == m:
+                    continue
+                p0 = (end[v - 1][m] if v else 0) // P
+                lim = min(lens[m], lens[l]) // P
+                k = lim
+                for j in range(p0, lim):
+                    if table[m][j] != table[l][j]:
+                        k = j
+                        break
+                kmin[l] = min(kmin.get(l, k), k)
+                cnt[l] += 1
+            for b in range(B):
+                l = leads[b]
+                start = end[v - 1][b] if v else 0
+                kept = l >= 0 and cnt[l] >= 1 and kmin[l] > start // P
+                lead[v][b] = l if kept else -1
+                end[v][b] = kmin[l] * P if kept else start
+                num[v][b] = cnt[b] + 1 if kept and l == b else 0
         tot_sh = 0
-        for l in range(B):
-            if lead[l] == l and shared[l] > 0:
-                members = cnt[l] + 1
-                for s0 in range(0, members, cap):
-                    subgroups.append((l, min(cap, members - s0), shared[l]))
-                tot_sh += ceil_div(members, cap) * shared[l]
+        for v in range(LEVELS):
+            for l in range(B):
+                if lead[v][l] == l:
+                    start = end[v - 1][l] if v else 0
+                    tot_sh += ceil_div(num[v][l], cap) * (end[v][l] - start)
         if forced_split <= 0 and tot_sh > 0:
             per = ceil_div(tot_sh * caps["hkv"], caps["prefix_grid"])
             per = ceil_div(per, 64) * 64
             C = max(C, per)
+    shared = [end[LEVELS - 1][b] if grouping else 0 for b in range(B)]
+    nsh = [0] * B
+    items = 0
+    if grouping:
+        for v in range(LEVELS):
+            for b in range(B):
+                if lead[v][b] >= 0:
+                    start = end[v - 1][b] if v else 0
+                    nsh[b] += ceil_div(end[v][b] - start, C)
+                    if lead[v][b] == b:
+                        items += ceil_div(num[v][b], cap) * ceil_div(end[v][b] - start, C)
     priv = [ceil_div(lens[b] - shared[b], TILE) for b in range(B)]
     pref = np.concatenate([[0], np.cumsum(priv)]).astype(np.int64)
     W = int(pref[-1])
@@ -94,15 +116,29 @@ def plan_decode(lens, table, P, caps, forced_split):
 
     slots = 0
     for b in range(B):
-        S = shared[b]
-        nsh = ceil_div(S, C) if S > 0 else 0
         p0, p1 = int(pref[b]), int(pref[b + 1])
         npriv = 1 + starts_before(p1) - starts_before(p0 + 1) if p1 > p0 else 0
-        direct = S == 0 and npriv == 1
+        direct = shared[b] == 0 and npriv == 1
         if not (direct or lens[b] == 0):
-            slots += nsh + npriv
-    items = sum(ceil_div(S, C) for (_, _, S) in subgroups)
+            slots += nsh[b] + npriv
     return items, slots, nwork
+
+
+def tree_batch(rng, P):
+    """Branching sessions: groups whose members share a prompt, with subsets sharing more."""
+    fan = [int(x) for x in rng.choice([2, 3, 4], size=int(rng.integers(1, 4)))]
+    sizes = []
+    size = int(np.prod(fan))
+    for f in fan:
+        sizes.append(size)
+        size //= f
+    levels = [(s, P * int(rng.integers(1, 20))) for s in sizes]
+    groups = int(rng.integers(1, max(2, 600 // sizes[0])))
+    base = sum(t for _, t in levels)
+    lens = [base + int(rng.integers(0, 3000)) for _ in range(groups * sizes[0])]
+    table, _, _ = wl._assign_tree_pages(rng, np.array(lens), P, levels)
+    order = rng.permutation(len(lens))
+    return [lens[i] for i in order], table[order]
 
 
 def group_batch(rng, groups, gsize, shared_pages, P, priv_hi):
@@ -142,13 +178,13 @@ def plain_batch(rng, B, P, kind):
 CONFIGS = []
 _rng = np.random.default_rng(2024)
 for i in range(160):
-    kind = ["ragged", "short", "uniform", "groups"][i % 4]
+    kind = ["ragged", "short", "uniform", "groups", "tree"][i % 5]
     P = int(_rng.choice([8, 16, 32, 64, 128]))
     hkv = int(_rng.choice([1, 2, 4, 8]))
     R = int(_rng.choice([1, 4, 8, 12, 16, 20]))
     n_tok = int(_rng.choice([1, 1, 2, 4, 8, 16, 64]))
     split = int(_rng.choice([0, 0, 0, 64, 256, 1024, 8192]))
-    B = int(_rng.choice([1, 7, 64, 128, 500, 1024, 1500, 3000])) if kind != "groups" else None
+    B = int(_rng.choice([1, 7, 64, 128, 500, 1024, 1500, 3000])) if kind not in ("groups", "tree") else None
     CONFIGS.append((i, kind, P, hkv, R, n_tok, split, B))
 
 
@@ -160,9 +196,11 @@ def test_decode_capacity_covers_planner(cfg):
         gsize = int(rng.choice([2, 3, 8, 20, 33]))
         groups = int(rng.integers(1, 1024 // gsize + 1))
         lens, table = group_batch(rng, groups, gsize, int(rng.integers(1, 40)), P, int(rng.integers(0, 5000)))
+    elif kind == "tree":
+        lens, table = tree_batch(rng, P)
     else:
         lens, table = plain_batch(rng, B, P, kind)
-    if kind != "groups" and B > 500 and kind == "ragged":
+    if kind == "ragged" and B > 500:
         lens = [min(x, 4096) for x in lens]        # keep the model fast on large batches
     B = len(lens)
     max_pages = table.shape[1]
@@ -214,3 +252,9 @@ def test_capacity_model_reaches_its_bounds():
     caps["hkv"] = 8
     items, slots, nwork = plan_decode(lens, table, 64, caps, 0)
     assert items > 0 and slots > 128
+    # a three-level tree: 16 groups of 8, halves and pairs sharing further pages
+    w = wl.decode_branching()
+    caps = ra.diag_decode_capacity(w.batch, 64, 8, w.block_table.shape[1], 64, 1, 0, True, 256, 1)
+    caps["hkv"] = 8
+    items_t, _, _ = plan_decode([int(x) for x in w.kv_lens], w.block_table, 64, caps, 0)
+    assert items_t >= 16 + 32 + 64       # at least one split per node of each level
