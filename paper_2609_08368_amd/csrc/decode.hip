@@ -171,14 +171,25 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
         }
       }
       __syncthreads();
+      bool kept = false;
       if (b < a.B) {
         const int lead = sLead[v][b];
-        const bool kept = lead >= 0 && sCnt[lead] >= 1 && sKmin[lead] > (start >> lg);
+        kept = lead >= 0 && sCnt[lead] >= 1 && sKmin[lead] > (start >> lg);
         sLead[v][b] = kept ? lead : -1;
         sEnd[v][b] = kept ? sKmin[lead] * P : start;
         sNum[v][b] = (kept && lead == b) ? sCnt[b] + 1 : 0;
       }
-      __syncthreads();
+      // no node at this level: none below it either
+      if (!__syncthreads_or(kept)) {
+        for (int w = v + 1; w < kPrefixLevels; ++w)
+          if (b < a.B) {
+            sLead[w][b] = -1;
+            sEnd[w][b] = sEnd[v][b];
+            sNum[w][b] = 0;
+          }
+        __syncthreads();
+        break;
+      }
     }
   }
   // keys [*t0, *t1) of sequence b shared at level v, if b is in a node there
