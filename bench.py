@@ -178,12 +178,24 @@ def pmc_workload(kind: str = "ragged"):
     fp8 = kind == "ragged-fp8"
     t = (wl.materialize_fp8 if fp8 else wl.materialize)(w, dev, poison=False)
     out = torch.empty_like(t["q"])
+    def calibrate():
+        src = torch.empty(CALIB_BYTES // 2, dtype=torch.bfloat16, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
     if kind == "extend":
         for _ in range(2):
             ra.extend_plain(t["q"], t["qo_indptr"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"],
                             t["scale"], out=out)
         torch.cuda.synchronize()
-        print(json.dumps({"pmc_workload": kind, "flops": w.flops()}), flush=True)
+        del t, out
+        torch.cuda.empty_cache()
+        calibrate()
+        print(json.dumps({"pmc_workload": kind, "flops": w.flops(), "kv_bytes": w.kv_bytes(),
+                          "calib_bytes": CALIB_BYTES}), flush=True)
         return
     share = {"prefix_share": not kind.endswith("-noshare")}
     if kind == "ragged-mtp4":
@@ -198,12 +210,7 @@ def pmc_workload(kind: str = "ragged"):
         else:
             ra.decode(t["q"], t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out,
                       **share)
-    src = torch.empty(CALIB_BYTES // 2, dtype=torch.bfloat16, device=dev).fill_(1.0)
-    dst = torch.empty_like(src)
-    torch.cuda.synchronize()
-    for _ in range(3):
-        dst.copy_(src)
-    torch.cuda.synchronize()
+    calibrate()
     per_elem = 0.5 if fp8 else 1.0     # kv_bytes() counts bf16 elements
     print(json.dumps({"pmc_workload": kind, "kv_bytes": int(w.kv_bytes(unique=True) * per_elem),
                       "logical_kv_bytes": int(w.kv_bytes() * per_elem), "calib_bytes": CALIB_BYTES}), flush=True)
@@ -263,17 +270,20 @@ def summarize_counters(d: str):
         print(f"{kern[-40:]:40s} {ctr:32s} dispatches {len(vals):3d}  mean {sum(vals) / len(vals):.6g}")
 
 
-def summarize_pmc(fetch_dir: str, write_dir: str, fp8: bool = False):
+def summarize_pmc(fetch_dir: str, write_dir: str, fp8: bool = False, extend: bool = False):
     """Turn the FETCH_SIZE and WRITE_SIZE runs into the committed traffic summary
-    (``fp8``: runs of the ``ragged-fp8`` workload)."""
+    (``fp8``: runs of the ``ragged-fp8`` workload; ``extend``: of the ``extend``
+    workload)."""
     import csv
     import glob
 
     from paper_2609_08368_amd import workloads as wl
 
+    kname = "extend_mfma_kernel" if extend else "decode_mfma_kernel"
+
     def per_kernel(d, counter):
-        # KiB per dispatch of the decode kernel, and of the calibration copies
-        # (the copy dispatches issued after the last decode dispatch)
+        # KiB per dispatch of the attention kernel, and of the calibration copies
+        # (the copy dispatches issued after the last attention dispatch)
         rows = []
         for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
             rows += [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
@@ -281,10 +291,14 @@ def summarize_pmc(fetch_dir: str, write_dir: str, fp8: bool = False):
         for r in rows:
             key = (int(r["Dispatch_Id"]), r["Kernel_Name"])
             per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
-        dec = {k: v for k, v in per.items() if "decode_mfma_kernel" in k[1]}
+        dec = {k: v for k, v in per.items() if kname in k[1]}
         last_dec = max(k[0] for k in dec)
         cal = {k: v for k, v in per.items() if "copy" in k[1].lower() and k[0] > last_dec}
         return {"decode": sum(dec.values()) / len(dec), "copy": sum(cal.values()) / len(cal)}
+
+    if extend:
+        return summarize_extend_pmc(per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE"),
+                                    fetch_dir.rstrip("/"), write_dir.rstrip("/"))
 
     fetch = per_kernel(fetch_dir, "FETCH_SIZE")
     write = per_kernel(write_dir, "WRITE_SIZE")
@@ -350,6 +364,56 @@ worker plus one per sequence). `bench.py` reports this traffic figure only while
 sources hash to the value recorded in `{json_name}` (sources under csrc/ plus build.py;
 hash {d['source_hash']}).
 """
+
+
+EXTEND_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "extend_multiturn_hbm_traffic.json")
+
+
+def summarize_extend_pmc(fetch: dict, write: dict, fetch_dir: str, write_dir: str):
+    """The extend kernel's HBM traffic summary from the calibrated counter means."""
+    from paper_2609_08368_amd import workloads as wl
+
+    w = wl.extend_multiturn()
+    f_scale = CALIB_BYTES / (fetch["copy"] * 1024.0)
+    w_scale = CALIB_BYTES / (write["copy"] * 1024.0)
+    rd = fetch["decode"] * 1024.0 * f_scale
+    wr = write["decode"] * 1024.0 * w_scale
+    q_bytes = w.total_q * w.hq * 128 * 2
+    res = {"kernel": "extend_mfma_kernel<false, 0>", "workload": "multi-turn extend batch (B32, Hq64/Hkv8, page 64)",
+           "source_hash": kernel_source_hash(), "fetch_kib_per_dispatch": fetch["decode"],
+           "write_kib_per_dispatch": write["decode"], "copy_fetch_kib": fetch["copy"], "copy_write_kib": write["copy"],
+           "fetch_scale": f_scale, "write_scale": w_scale, "hbm_read_bytes": rd, "hbm_write_bytes": wr,
+           "kv_bytes": w.kv_bytes(), "q_bytes": q_bytes, "out_bytes": q_bytes,
+           "read_over_kv_plus_q": rd / (w.kv_bytes() + q_bytes), "write_over_out": wr / q_bytes}
+    with open(EXTEND_TRAFFIC_FILE, "w") as f:
+        json.dump(res, f, indent=1)
+    with open(EXTEND_TRAFFIC_FILE[:-5] + ".md", "w") as f:
+        f.write(f"""# HBM traffic of {res['kernel']} on the multi-turn extend batch
+
+Workload: B 32, cached prefix U{{8192..65536}}, chunk U{{64..2048}}, Hq 64 / Hkv 8, page 64;
+36,098 chunk rows. Every K and V byte a sequence needs, read once: {res['kv_bytes']:,} B; q
+{q_bytes:,} B read and out {q_bytes:,} B written.
+
+Commands (repo root, one MI355X), one counter per pass:
+
+    rocprofv3 --pmc FETCH_SIZE --output-format csv -d {fetch_dir} -o run -- python bench.py --pmc-workload extend
+    rocprofv3 --pmc WRITE_SIZE --output-format csv -d {write_dir} -o run -- python bench.py --pmc-workload extend
+    python bench.py --summarize-pmc {fetch_dir} {write_dir} --extend
+
+`--pmc-workload extend` runs two extend launches, then three 2 GiB device copies that
+calibrate the counters (FETCH_SIZE scale {f_scale:.3f}, WRITE_SIZE scale {w_scale:.3f}).
+
+| counter | raw KiB / dispatch | scaled bytes | reading |
+|---|---|---|---|
+| FETCH_SIZE | {fetch['decode']:,.0f} | {rd:,.0f} | {res['read_over_kv_plus_q']:.3f} x (KV + q) |
+| WRITE_SIZE | {write['decode']:,.0f} | {wr:,.0f} | {res['write_over_out']:.3f} x out |
+
+The kernel is bound by the matrix cores, not by HBM: at about 42 ms per launch these bytes move
+at about {(rd + wr) / 42e-3 / 1e9:,.0f} GB/s. The work units of one (sequence, KV head) run
+on one XCD and share their keys through its L2, so the keys beyond the first unit's reads
+mostly come from L2. Sources hash {res['source_hash']}.
+""")
+    print(json.dumps(res, indent=1))
 
 
 def traffic_bytes(fp8: bool = False):
@@ -565,9 +629,10 @@ def main():
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the HBM traffic summary from two rocprofv3 --pmc output directories")
     ap.add_argument("--fp8", action="store_true", help="with --summarize-pmc: runs of --pmc-workload ragged-fp8")
+    ap.add_argument("--extend", action="store_true", help="with --summarize-pmc: runs of --pmc-workload extend")
     args = ap.parse_args()
     if args.summarize_pmc:
-        summarize_pmc(*args.summarize_pmc, fp8=args.fp8)
+        summarize_pmc(*args.summarize_pmc, fp8=args.fp8, extend=args.extend)
         return
     if args.pmc_workload:
         pmc_workload(args.pmc_workload)

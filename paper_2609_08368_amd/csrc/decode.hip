@@ -69,7 +69,9 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
   // small batches (one sequence per thread) keep per-sequence state in LDS
   // and get trajectory-group detection
   const bool small = a.B <= kGroupMax;
-  const bool grouping = a.group_cap >= 2 && small;
+  // grouping: the batch is searched for shared prefix pages; it stays on only
+  // if a node is found
+  bool grouping = a.group_cap >= 2 && small;
   const uint32_t bt_sj = (uint32_t)a.kv.bt_sj;
   int bad = 0, cap_bad = 0;
 
@@ -179,8 +181,13 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
         sEnd[v][b] = kept ? sKmin[lead] * P : start;
         sNum[v][b] = (kept && lead == b) ? sCnt[b] + 1 : 0;
       }
-      // no node at this level: none below it either
+      // no node at this level: none below it either (and with none at the
+      // first level the batch has no shared pages at all)
       if (!__syncthreads_or(kept)) {
+        if (v == 0) {
+          grouping = false;
+          break;
+        }
         for (int w = v + 1; w < kPrefixLevels; ++w)
           if (b < a.B) {
             sLead[w][b] = -1;
