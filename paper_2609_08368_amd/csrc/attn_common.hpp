@@ -193,17 +193,51 @@ __device__ __forceinline__ uint64_t row_offset(uint32_t pg, uint32_t sp, int slo
   return (uint64_t)pg * sp + __umul24((uint32_t)slot, ss);
 }
 
+// Inclusive prefix sums over a wave's 64 lanes, without LDS: DPP row shifts
+// (row_shr 1, 2, 4, 8; lanes shifted in from outside the 16-lane row read 0)
+// scan each row, then each row adds the totals of the rows below it, read from
+// lanes 15, 31 and 47. Every lane of the wave must be active.
+template <int kCtrl>
+__device__ __forceinline__ int dpp_shr(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, kCtrl, 0xf, 0xf, true);
+}
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+  x += dpp_shr<0x111>(x);
+  x += dpp_shr<0x112>(x);
+  x += dpp_shr<0x114>(x);
+  x += dpp_shr<0x118>(x);
+  const int r0 = __builtin_amdgcn_readlane(x, 15), r1 = __builtin_amdgcn_readlane(x, 31);
+  const int r2 = __builtin_amdgcn_readlane(x, 47);
+  const int row = (threadIdx.x & 63) >> 4;
+  return x + (row >= 1 ? r0 : 0) + (row >= 2 ? r1 : 0) + (row >= 3 ? r2 : 0);
+}
+template <int kCtrl>
+__device__ __forceinline__ long long dpp_shr64(long long v) {
+  const uint32_t lo = (uint32_t)dpp_shr<kCtrl>((int)(uint32_t)v);
+  const uint32_t hi = (uint32_t)dpp_shr<kCtrl>((int)(uint32_t)((unsigned long long)v >> 32));
+  return (long long)(((unsigned long long)hi << 32) | lo);
+}
+__device__ __forceinline__ long long readlane64(long long v, int lane) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((unsigned long long)v >> 32), lane);
+  return (long long)(((unsigned long long)hi << 32) | lo);
+}
+__device__ __forceinline__ long long wave_inclusive_scan64(long long x) {
+  x += dpp_shr64<0x111>(x);
+  x += dpp_shr64<0x112>(x);
+  x += dpp_shr64<0x114>(x);
+  x += dpp_shr64<0x118>(x);
+  const long long r0 = readlane64(x, 15), r1 = readlane64(x, 31), r2 = readlane64(x, 47);
+  const int row = (threadIdx.x & 63) >> 4;
+  return x + (row >= 1 ? r0 : 0) + (row >= 2 ? r1 : 0) + (row >= 3 ? r2 : 0);
+}
+
 // Exclusive prefix sum over the calling block (all threads must call it);
 // wave_tot is a 16-int LDS scratch array. Returns this thread's exclusive sum
 // and the block total in *total.
 __device__ __forceinline__ int block_exclusive_scan(int v, int* total, int* wave_tot) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
+  const int x = wave_inclusive_scan(v);
   if (lane == 63) wave_tot[wave] = x;
   __syncthreads();
   int before = 0, all = 0;
@@ -221,12 +255,7 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* total, int* wave
 // 64-bit version of block_exclusive_scan (wave_tot: 16 slots).
 __device__ __forceinline__ long long block_exclusive_scan64(long long v, long long* total, long long* wave_tot) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  long long x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const long long y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
+  const long long x = wave_inclusive_scan64(v);
   if (lane == 63) wave_tot[wave] = x;
   __syncthreads();
   long long before = 0, all = 0;

@@ -32,6 +32,8 @@ constexpr int kTile = 32;          // keys per inner iteration of the private ke
 constexpr int kGroupMax = 1024;    // batches up to this size get trajectory-group detection
 constexpr int kIntMax = 0x7fffffff;
 constexpr int kHashBits = 11;     // planner hash table: 2048 slots for up to kGroupMax (parent, page) keys
+constexpr int kCmpUnroll = 8;     // block-table entries a lane compares per round
+static_assert(kPrefixLevels * 16 <= 62, "per-level sub-group counts are packed in 16-bit fields");
 
 __device__ __forceinline__ int clamp_len(int L, int max_tokens, int* bad) {
   if (L < 0 || L > max_tokens) {
@@ -42,6 +44,32 @@ __device__ __forceinline__ int clamp_len(int L, int max_tokens, int* bad) {
 }
 
 __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// Exclusive scan of v over the workgroup, with the totals of v and of w, in
+// one pair of barriers (wave_tot: 32 slots).
+__device__ __forceinline__ long long block_scan_sum64(long long v, long long w, long long* tot_v, long long* tot_w,
+                                                      long long* wave_tot) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const long long x = wave_inclusive_scan64(v);
+  w = wave_inclusive_scan64(w);
+  if (lane == 63) {
+    wave_tot[wave] = x;
+    wave_tot[16 + wave] = w;
+  }
+  __syncthreads();
+  long long before = 0, all = 0, all_w = 0;
+  const int nw = blockDim.x >> 6;
+  for (int i = 0; i < nw; ++i) {
+    const long long t = wave_tot[i];
+    if (i < wave) before += t;
+    all += t;
+    all_w += wave_tot[16 + i];
+  }
+  __syncthreads();
+  *tot_v = all;
+  *tot_w = all_w;
+  return before + x - v;
+}
 
 // Key of the planner's hash table: (parent node leader + 1, page id); ~0 = empty.
 __device__ __forceinline__ unsigned long long node_key(int parent, int page) {
@@ -62,7 +90,11 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
   __shared__ unsigned long long hKey[1 << kHashBits];
   __shared__ int hMin[1 << kHashBits];
   __shared__ int wave_tot[16];
-  __shared__ long long wsum[16];
+  __shared__ long long wsum[32];
+  // small batches: the private prefix sums, and per sub-group (first key,
+  // first slot offset, end key, splits), kept here for the later phases
+  __shared__ long long sPref[kGroupMax + 1];
+  __shared__ int4 sSgInfo[kPrefixLevels * kGroupMax];
   const int tid = threadIdx.x, nthr = blockDim.x, lane = tid & 63, wave = tid >> 6, nwaves = nthr >> 6;
   const int lg = a.kv.log2_page, P = a.kv.page_size;
   const int max_tokens = a.kv.max_pages * P;
@@ -75,6 +107,10 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
   const uint32_t bt_sj = (uint32_t)a.kv.bt_sj;
   int bad = 0, cap_bad = 0;
 
+  // the first page id of every sequence (the key of level 0 of the search
+  // below) is read with the lengths, so the two loads share one wait
+  const int page0 = grouping && tid < a.B && a.kv.max_pages > 0 ? a.kv.bt[(int64_t)tid * a.kv.bt_sb] : 0;
+
   // lengths and their sum
   long long sum = 0;
   for (int b = tid; b < a.B; b += nthr) {
@@ -82,9 +118,8 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
     sum += L;
     if (small) sL[b] = L;
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
-  if (lane == 0) wsum[wave] = sum;
+  sum = wave_inclusive_scan64(sum);
+  if (lane == 63) wsum[wave] = sum;
   __syncthreads();
   long long total = 0;
   for (int w = 0; w < nwaves; ++w) total += wsum[w];
@@ -107,6 +142,11 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
   // such page. Its keys [parent end, node end) are then read once for all its
   // members by the group-prefix pass.
   if (grouping) {
+    // lanes per member in the comparisons: the most (up to a wave) that still
+    // cover the whole batch with the workgroup's threads
+    int lpm_log = 6;
+    while (lpm_log > 0 && (a.B << lpm_log) > nthr) --lpm_log;
+    const int lpm = 1 << lpm_log;
     for (int v = 0; v < kPrefixLevels; ++v) {
       for (int i = tid; i < (1 << kHashBits); i += nthr) {
         hKey[i] = ~0ull;
@@ -123,7 +163,9 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
       // takes part: in a node at the previous level (or at level 0), with a
       // full page at the position that follows the shared range
       const bool part = b < a.B && (v == 0 || parent >= 0) && (sL[b] >> lg) > (start >> lg);
-      const int page = part ? a.kv.bt[(int64_t)b * a.kv.bt_sb + (int64_t)__umul24((uint32_t)(start >> lg), bt_sj)] : 0;
+      const int page = !part ? 0
+                       : v == 0 ? page0
+                                : a.kv.bt[(int64_t)b * a.kv.bt_sb + (int64_t)__umul24((uint32_t)(start >> lg), bt_sj)];
       const unsigned long long key = node_key(parent, page);
       if (part) {
         int h = key_hash(key);
@@ -148,26 +190,50 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
       }
       __syncthreads();
       // leading full pages each member shares with its leader from the parent's
-      // end on (one wave per member, 64 pages per comparison); the node shares
-      // the minimum
-      for (int m = wave; m < a.B; m += nwaves) {
-        const int lead = sLead[v][m];
-        if (lead < 0 || lead == m) continue;
-        const int p0 = (v == 0 ? 0 : sEnd[v - 1][m]) >> lg;
-        const int lim = min(sL[m], sL[lead]) >> lg;
-        const int* rb = a.kv.bt + (int64_t)m * a.kv.bt_sb;
-        const int* rl = a.kv.bt + (int64_t)lead * a.kv.bt_sb;
+      // end on; the node shares the minimum. All members are compared at once:
+      // an aligned group of lpm lanes per member, each lane checking
+      // kCmpUnroll entries per round (lane s: entries c + s + lpm u), so a
+      // round covers lpm * kCmpUnroll pages of every member and costs one
+      // round trip to the block table
+      for (int m0 = 0; m0 < a.B; m0 += nthr >> lpm_log) {
+        const int m = m0 + (tid >> lpm_log), sub = tid & (lpm - 1);
+        const int lead = m < a.B ? sLead[v][m] : -1;
+        const bool member = lead >= 0 && lead != m;
+        const int p0 = member ? (v == 0 ? 0 : sEnd[v - 1][m]) >> lg : 0;
+        // both rows hold full pages at p0 (they took part), so lim > p0; the
+        // test keeps every index read below in [p0, lim) regardless
+        const int lim = member ? min(sL[m], sL[lead]) >> lg : 0;
+        bool active = member && lim > p0;
+        const int* rb = a.kv.bt + (int64_t)(member ? m : 0) * a.kv.bt_sb;
+        const int* rl = a.kv.bt + (int64_t)(member ? lead : 0) * a.kv.bt_sb;
         int k = lim;
-        for (int c = p0; c < lim; c += 64) {
-          const int kk = c + lane;
-          const bool differ = kk < lim && rb[__umul24((uint32_t)kk, bt_sj)] != rl[__umul24((uint32_t)kk, bt_sj)];
-          const unsigned long long mask = __builtin_amdgcn_ballot_w64(differ);
-          if (mask) {
-            k = c + __builtin_ctzll(mask);
-            break;
+        for (int c = p0; __builtin_amdgcn_ballot_w64(active) != 0; c += lpm * kCmpUnroll) {
+          int found = kIntMax;
+          if (active) {
+            int x[kCmpUnroll], y[kCmpUnroll];
+#pragma unroll
+            for (int u = 0; u < kCmpUnroll; ++u) {
+              const int kk = min(c + sub + lpm * u, lim - 1);
+              x[u] = rb[__umul24((uint32_t)kk, bt_sj)];
+              y[u] = rl[__umul24((uint32_t)kk, bt_sj)];
+            }
+#pragma unroll
+            for (int u = 0; u < kCmpUnroll; ++u) {
+              const int kk = c + sub + lpm * u;
+              if (kk < lim && x[u] != y[u]) found = min(found, kk);
+            }
+          }
+          for (int o = 1; o < lpm; o <<= 1) found = min(found, __shfl_xor(found, o, 64));
+          if (active) {
+            if (found != kIntMax) {
+              k = found;
+              active = false;
+            } else if (c + lpm * kCmpUnroll >= lim) {
+              active = false;
+            }
           }
         }
-        if (lane == 0) {
+        if (member && sub == 0) {
           atomicMin(&sKmin[lead], k);
           atomicAdd(&sCnt[lead], 1);
         }
@@ -213,18 +279,24 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
   // nodes' leaders, level after level
   int n_sg = 0;
   if (grouping) {
-    long long tot_sh = 0;
+    // one scan for all levels: the per-level counts of a leader are packed in
+    // 16-bit fields (a level's total is at most B <= kGroupMax, so no field
+    // carries into the next), beside the sum of shared keys times sub-groups
+    const int b = tid;
+    long long packed = 0, keys = 0;
     for (int v = 0; v < kPrefixLevels; ++v) {
-      const int b = tid;
-      int nsub = 0, t0 = 0, t1 = 0;
-      if (b < a.B && level_range(v, b, &t0, &t1) && sLead[v][b] == b) nsub = ceil_div(sNum[v][b], cap);
-      int tot;
-      const int excl = block_exclusive_scan(nsub, &tot, wave_tot);
-      if (b < a.B) sSg[v][b] = n_sg + excl;
-      n_sg += tot;
-      long long tsh;
-      (void)block_exclusive_scan64(nsub > 0 ? (long long)nsub * (t1 - t0) : 0, &tsh, wsum);
-      tot_sh += tsh;
+      int t0 = 0, t1 = 0;
+      if (b < a.B && level_range(v, b, &t0, &t1) && sLead[v][b] == b) {
+        const int nsub = ceil_div(sNum[v][b], cap);
+        packed += (long long)nsub << (16 * v);
+        keys += (long long)nsub * (t1 - t0);
+      }
+    }
+    long long tot_packed, tot_sh;
+    const long long excl = block_scan_sum64(packed, keys, &tot_packed, &tot_sh, wsum);
+    for (int v = 0; v < kPrefixLevels; ++v) {
+      if (b < a.B) sSg[v][b] = n_sg + (int)((excl >> (16 * v)) & 0xFFFF);
+      n_sg += (int)((tot_packed >> (16 * v)) & 0xFFFF);
     }
     // Split of the shared keys: at least C, and large enough that the shared
     // items of all sub-groups times the KV heads fit the group-prefix grid in
@@ -264,7 +336,10 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
     }
     long long tot;
     const long long ex = poff + block_exclusive_scan64(priv, &tot, wsum);
-    if (b < a.B) a.ws.pref[b] = ex;
+    if (b < a.B) {
+      a.ws.pref[b] = ex;
+      if (small) sPref[b] = ex;
+    }
     poff += tot;
   }
   const long long W = poff;
@@ -274,7 +349,10 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
     const long long n = (W + per - 1) / per;
     nwork = (int)(n < a.max_workers ? n : a.max_workers);
   }
-  if (tid == 0) a.ws.pref[a.B] = W;
+  if (tid == 0) {
+    a.ws.pref[a.B] = W;
+    if (small) sPref[a.B] = W;
+  }
   __syncthreads();   // prefix sums visible to the workgroup
   // workers whose share starts before tile y of the concatenation (0 < y <= W)
   auto starts_before = [&](long long y) -> long long { return (y * nwork + W - 1) / W; };
@@ -292,7 +370,7 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
       L = small ? sL[b] : clamp_len(a.lens[b * a.lens_s], max_tokens, &dummy);
       S = shared_keys(b);
       nsh = shared_splits(b);
-      const long long p0 = a.ws.pref[b], p1 = a.ws.pref[b + 1];
+      const long long p0 = small ? sPref[b] : a.ws.pref[b], p1 = small ? sPref[b + 1] : a.ws.pref[b + 1];
       npriv = p1 > p0 ? (int)(1 + starts_before(p1) - starts_before(p0 + 1)) : 0;
       empty = L == 0;
       direct = S == 0 && npriv == 1;
@@ -323,6 +401,7 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
         if (pos == 0) {
           a.ws.sgroups[sg] = make_int4(b, min(cap, sNum[v][lead] - (rank / cap) * cap), t1, n_split);
           a.ws.sg_range[sg] = make_int2(t0, off);
+          sSgInfo[sg] = make_int4(t0, off, t1, n_split);
         }
         off += n_split;
       }
@@ -335,21 +414,16 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
   int sitem_off = 0;
   for (int g0 = 0; g0 < n_sg; g0 += nthr) {
     const int sg = g0 + tid;
-    int4 info = make_int4(0, 0, 0, 0);
-    int2 rng = make_int2(0, 0);
-    if (sg < n_sg) {
-      info = a.ws.sgroups[sg];
-      rng = a.ws.sg_range[sg];
-    }
+    // (first key, first slot offset, end key, splits)
+    const int4 info = sg < n_sg ? sSgInfo[sg] : make_int4(0, 0, 0, 0);
     int tot;
-    const int base = sitem_off + block_exclusive_scan(sg < n_sg ? info.w : 0, &tot, wave_tot);
-    if (sg < n_sg)
-      for (int s = 0; s < info.w; ++s) {
-        if (base + s < a.max_items)
-          a.ws.sitems[base + s] = make_int4(sg, rng.x + s * C, min(info.z, rng.x + (s + 1) * C), rng.y + s);
-        else
-          cap_bad = 1;
-      }
+    const int base = sitem_off + block_exclusive_scan(info.w, &tot, wave_tot);
+    for (int s = 0; s < info.w; ++s) {
+      if (base + s < a.max_items)
+        a.ws.sitems[base + s] = make_int4(sg, info.x + s * C, min(info.z, info.x + (s + 1) * C), info.y + s);
+      else
+        cap_bad = 1;
+    }
     sitem_off += tot;
   }
   if (tid == 0) {
