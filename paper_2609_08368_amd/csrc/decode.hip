@@ -973,17 +973,37 @@ __global__ __launch_bounds__(kPrefixWaves * 64, 2) void prefix_kernel(DecodeArgs
 __device__ __forceinline__ void merge_parts(const float* o_base, int64_t o_step, const float* l_base, int64_t l_step,
                                             int n, float* out2, float* lse_out) {
   const int lane = threadIdx.x & 63;
-  float M = kNegInf;
-  for (int s0 = 0; s0 < n; s0 += 64)
+  // The o rows of the first kPre parts are loaded together with the lse
+  // values, so a row of at most kPre parts (the usual case) waits for one
+  // round trip instead of two.
+  constexpr int kPre = 4;
+  float2 pre[kPre];
+#pragma unroll
+  for (int u = 0; u < kPre; ++u)
+    pre[u] = u < n ? *reinterpret_cast<const float2*>(o_base + (int64_t)u * o_step + 2 * lane) : make_float2(0.f, 0.f);
+  const float l0 = lane < n ? l_base[(int64_t)lane * l_step] : kNegInf;
+  float M = l0;
+  for (int s0 = 64; s0 < n; s0 += 64)
     if (s0 + lane < n) M = fmaxf(M, l_base[(int64_t)(s0 + lane) * l_step]);
   M = wave_max(M);
   float z = 0.f, a0 = 0.f, a1 = 0.f;
   if (M != kNegInf) {
     for (int s0 = 0; s0 < n; s0 += 64) {
-      const float my_w = s0 + lane < n ? exp2_fast((l_base[(int64_t)(s0 + lane) * l_step] - M) * kLog2e) : 0.f;
+      const float lv = s0 == 0 ? l0 : (s0 + lane < n ? l_base[(int64_t)(s0 + lane) * l_step] : kNegInf);
+      const float my_w = s0 + lane < n ? exp2_fast((lv - M) * kLog2e) : 0.f;
       z += my_w;
       const int cnt = min(64, n - s0);
       int s = 0;
+      if (s0 == 0) {
+#pragma unroll
+        for (int u = 0; u < kPre; ++u)
+          if (u < cnt) {
+            const float w = __shfl(my_w, u, 64);
+            a0 += w * pre[u].x;
+            a1 += w * pre[u].y;
+          }
+        s = min(cnt, kPre);
+      }
       for (; s + 4 <= cnt; s += 4) {
         float2 v[4];
 #pragma unroll
@@ -1016,13 +1036,14 @@ __global__ __launch_bounds__(64) void combine_kernel(DecodeArgs a) {
   const int b = blockIdx.x / a.Hv;
   const int hv = blockIdx.x - b * a.Hv;
   const int tok = hv / a.Hq, h = hv - tok * a.Hq;
+  // the planner writes both for every sequence; they are read together
   const int n = a.ws.nparts[b];
+  const int base = a.ws.base[b];
   if (n == 0) return;     // written directly by its only piece
   float r[2] = {0.f, 0.f}, lse_v = kNegInf;   // an empty sequence (n == -1): zeros, -inf
   if (n == -2) {          // its slots did not fit the workspace (reported as kErrCapacity)
     r[0] = r[1] = lse_v = __uint_as_float(0x7fc00000u);   // a quiet NaN
   } else if (n > 0) {
-    const int base = a.ws.base[b];
     merge_parts(a.ws.part_o + ((int64_t)base * a.Hv + hv) * kHeadDim, (int64_t)a.Hv * kHeadDim,
                 a.ws.part_lse + (int64_t)base * a.Hv + hv, a.Hv, n, r, &lse_v);
   }
