@@ -108,8 +108,8 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
         bad = 1;
         pg = pg < 0 ? 0 : kv.num_pages - 1;
       }
-      kr[i] = load_kv_raw<kFp8>(kbase + ES * row_offset((uint32_t)pg, ksp, t & pmask, kss));
-      vr[i] = load_kv_raw<kFp8>(vbase + ES * row_offset((uint32_t)pg, vsp, t & pmask, vss));
+      kr[i] = load_kv_raw_nt<kFp8>(kbase + ES * row_offset((uint32_t)pg, ksp, t & pmask, kss));
+      vr[i] = load_kv_raw_nt<kFp8>(vbase + ES * row_offset((uint32_t)pg, vsp, t & pmask, vss));
     }
   };
   auto stage = [&](int buf, const Rows& kr, const Rows& vr) {
