@@ -517,21 +517,20 @@ struct RowPart<true> {
 
 // Split-KV decode on MFMA for a packed GQA group of up to 16 query heads.
 // One wave per (private item, KV head, 16-head block). Keys are processed 32
-// at a time. With bf16 pages of at least 32 keys, K and V rows are loaded
-// whole (16 lanes per 256-byte row, four rows per instruction) with
-// non-temporal loads and staged in the wave's own LDS tiles; K is read back
-// as the A operand of S^T = K Q^T and V transposed as the A operand of
-// O^T += V^T P^T. Measured on the ragged 64K batch: 1.53-1.56 ms per kernel
-// (6.7-6.8 TB/s) against 1.68-1.69 ms for K loaded straight into A-operand
-// registers (each lane its RowPart of a row: 64-byte pieces per instruction,
-// which non-temporal loads fetch again per piece) and V staged the same way.
-// FP8 pages and pages of fewer than 32 keys keep that path (FP8 whole rows
-// measured 4% slower). Rows are fetched one tile ahead (bf16) or two (FP8),
-// and page ids one tile ahead of the rows they address.
+// at a time. With pages of at least 32 keys, K and V rows are loaded whole
+// (every instruction reads whole rows) with non-temporal loads and staged in
+// the wave's own LDS tiles; K is read back as the A operand of S^T = K Q^T
+// and V transposed as the A operand of O^T += V^T P^T. Measured on the ragged
+// 64K batch: 1.50-1.56 ms per kernel (6.7-6.9 TB/s) against 1.68-1.69 ms with
+// K loaded straight into A-operand registers (each lane its RowPart of a row,
+// so an instruction reads 64-byte pieces of 16 rows, which non-temporal
+// loads fetch again per piece) and V staged the same way; FP8 pages 0.84
+// against 0.89 ms (with 8-byte loads, 16 lanes per row, 0.93 ms). Pages of
+// fewer than 32 keys keep the RowPart path. Rows are fetched one tile ahead
+// (bf16) or two (FP8), and page ids one tile ahead of the rows they address.
 template <bool kFp8>
 __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
-  // dynamic LDS: per wave a V tile and, with bf16 pages, a K tile (32 keys x
-  // 272 B each)
+  // dynamic LDS: per wave a V tile and a K tile (32 keys x 272 B each)
   extern __shared__ u16 vs_dyn[];
   typedef u16 VTile[kTile][kHeadDim + 8];
 
@@ -544,8 +543,8 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
   const int wave = threadIdx.x >> 6;
   const int rem = (blockIdx.x - worker * nch) * wpg + wave;
   // bf16 pages: a V tile and a K tile per wave; FP8 pages: a V tile
-  VTile& vs = reinterpret_cast<VTile*>(vs_dyn)[kFp8 ? wave : 2 * wave];
-  VTile& ks = reinterpret_cast<VTile*>(vs_dyn)[kFp8 ? wave : 2 * wave + 1];   // unused with FP8
+  VTile& vs = reinterpret_cast<VTile*>(vs_dyn)[2 * wave];
+  VTile& ks = reinterpret_cast<VTile*>(vs_dyn)[2 * wave + 1];
   const int g = rem % a.Hkv;
   const int qb = rem / a.Hkv;
   int bad = 0;
@@ -592,13 +591,16 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
     // FP8 rows are half the bytes, so they go two tiles ahead (the same bytes
     // and registers in flight as one bf16 tile).
     constexpr int kDepth = kFp8 ? 2 : 1;
-    // Rows in flight. kWhole (bf16 pages, one page per tile): whole rows, 16
-    // lanes per 256-byte row (lane l: elements 8 (l % 16) .. + 7 of rows
-    // 4 i + l / 16), loaded non-temporally and staged in LDS; otherwise each
-    // lane's RowPart of keys 16 hh + col, K kept in registers.
-    constexpr bool kWhole = kHolds && !kFp8;
+    // Rows in flight. kWhole (one page per tile): whole rows, loaded
+    // non-temporally 16 bytes per lane and staged in LDS; bf16: 16 lanes per
+    // 256-byte row (lane l: elements 8 (l % 16) .. + 7 of rows 4 i + l / 16),
+    // FP8: 8 lanes per 128-byte row (lane l: codes 16 (l % 8) .. + 15 of rows
+    // 8 i + l / 8). Otherwise each lane's RowPart of keys 16 hh + col, K kept
+    // in registers.
+    constexpr bool kWhole = kHolds;
+    typedef std::conditional_t<kFp8, uint4, bf16x8> Piece;
     struct WholeRows {
-      KvRaw<kFp8> r[8];
+      Piece r[kFp8 ? 4 : 8];
     };
     typedef std::conditional_t<kWhole, WholeRows, RowPart<kFp8>[2]> Rows;
     Rows kc0, kc1, vc0, vc1;
@@ -630,13 +632,14 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
           bad = 1;
           pg = pg < 0 ? 0 : a.kv.num_pages - 1;
         }
-        const int piece = 8 * (lane & 15);
+        constexpr int kRowsPer = kFp8 ? 8 : 4, kLanesPerRow = 64 / kRowsPer, kN = kFp8 ? 4 : 8;
+        const int piece = (kFp8 ? 16 : 8) * (lane & (kLanesPerRow - 1));
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          int t = t0 + 4 * i + (lane >> 4);
+        for (int i = 0; i < kN; ++i) {
+          int t = t0 + kRowsPer * i + lane / kLanesPerRow;
           t = t < t_end ? t : t_end - 1;
-          kc.r[i] = load_kv_raw_nt<kFp8>(kbase + ES * (row_offset((uint32_t)pg, ksp, t & pmask, kss) + piece));
-          vc.r[i] = load_kv_raw_nt<kFp8>(vbase + ES * (row_offset((uint32_t)pg, vsp, t & pmask, vss) + piece));
+          kc.r[i] = load_nt<Piece>(kbase + ES * (row_offset((uint32_t)pg, ksp, t & pmask, kss) + piece));
+          vc.r[i] = load_nt<Piece>(vbase + ES * (row_offset((uint32_t)pg, vsp, t & pmask, vss) + piece));
         }
       } else {
 #pragma unroll
@@ -664,10 +667,22 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
       if constexpr (kWhole) {
         // stage both tiles, then the rows kDepth tiles ahead take the
         // registers at once
+        if constexpr (kFp8) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          *reinterpret_cast<bf16x8*>(&vs[4 * i + (lane >> 4)][8 * (lane & 15)]) = kv_to_bf16x8<kFp8>(vc.r[i]);
-          *reinterpret_cast<bf16x8*>(&ks[4 * i + (lane >> 4)][8 * (lane & 15)]) = kv_to_bf16x8<kFp8>(kc.r[i]);
+          for (int i = 0; i < 4; ++i) {
+            const int row = 8 * i + (lane >> 3), e0 = 16 * (lane & 7);
+            const uint4 kw = kc.r[i], vw = vc.r[i];
+            *reinterpret_cast<bf16x8*>(&vs[row][e0]) = kv_to_bf16x8<true>(make_uint2(vw.x, vw.y));
+            *reinterpret_cast<bf16x8*>(&vs[row][e0 + 8]) = kv_to_bf16x8<true>(make_uint2(vw.z, vw.w));
+            *reinterpret_cast<bf16x8*>(&ks[row][e0]) = kv_to_bf16x8<true>(make_uint2(kw.x, kw.y));
+            *reinterpret_cast<bf16x8*>(&ks[row][e0 + 8]) = kv_to_bf16x8<true>(make_uint2(kw.z, kw.w));
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            *reinterpret_cast<bf16x8*>(&vs[4 * i + (lane >> 4)][8 * (lane & 15)]) = kv_to_bf16x8<kFp8>(vc.r[i]);
+            *reinterpret_cast<bf16x8*>(&ks[4 * i + (lane >> 4)][8 * (lane & 15)]) = kv_to_bf16x8<kFp8>(kc.r[i]);
+          }
         }
         fetch_rows(tn, kc, vc);
         fetch_pages(tn + kTile);
@@ -1156,7 +1171,7 @@ void launch_decode_kernels(const DecodeArgs& a, hipStream_t stream, KernelTimer*
   } else {
     const unsigned nch = per_item / a.item_waves;
     const unsigned grid = (unsigned)((int64_t)a.max_workers * nch);
-    const size_t lds = (size_t)(kFp8 ? 1 : 2) * a.item_waves * kTile * (kHeadDim + 8) * sizeof(u16);
+    const size_t lds = (size_t)2 * a.item_waves * kTile * (kHeadDim + 8) * sizeof(u16);
     decode_mfma_kernel<kFp8><<<grid, 64 * a.item_waves, lds, stream>>>(a);
   }
   if (timer) (void)hipEventRecord(timer->stop, stream);
@@ -1172,7 +1187,7 @@ int workers_per_cu_of(int R, int Hkv, int item_waves, int n_tok) {
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_valu_kernel<kFp8>, 64, 0) != hipSuccess) blocks = 0;
     return blocks / Hkv > 1 ? blocks / Hkv : 1;
   }
-  const size_t lds = (size_t)(kFp8 ? 1 : 2) * item_waves * kTile * (kHeadDim + 8) * sizeof(u16);
+  const size_t lds = (size_t)2 * item_waves * kTile * (kHeadDim + 8) * sizeof(u16);
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, decode_mfma_kernel<kFp8>, 64 * item_waves, lds) != hipSuccess)
     blocks = 0;
   const int nch = Hkv * ((R + 15) / 16) / item_waves;
