@@ -98,13 +98,22 @@ __global__ __launch_bounds__(kAppendThreads) void append_kernel(AppendArgs a) {
   const int g0 = (rem / (kHeadDim / 8)) * kGroup, c = rem % (kHeadDim / 8);
   const int gn = min(kGroup, a.Hkv - g0);
   // the new rows are read first (always in bounds), so their latency overlaps
-  // the lookups below
+  // the lookups below; into bf16 pages they are read non-temporally (the
+  // multi-turn batch's 36,098 chunk rows: 54 -> 50 us; into FP8 pages the same
+  // loads measured 4% slower, and non-temporal page stores gained nothing)
   bf16x8 kx[kGroup], vx[kGroup];
 #pragma unroll
   for (int j = 0; j < kGroup; ++j) {
     const int g = g0 + (j < gn ? j : 0);
-    kx[j] = *reinterpret_cast<const bf16x8*>((const __bf16*)a.k_new + r * a.kn_st + g * a.kn_sh + 8 * c);
-    vx[j] = *reinterpret_cast<const bf16x8*>((const __bf16*)a.v_new + r * a.vn_st + g * a.vn_sh + 8 * c);
+    const __bf16* kp = (const __bf16*)a.k_new + r * a.kn_st + g * a.kn_sh + 8 * c;
+    const __bf16* vp = (const __bf16*)a.v_new + r * a.vn_st + g * a.vn_sh + 8 * c;
+    if constexpr (kFp8) {
+      kx[j] = *reinterpret_cast<const bf16x8*>(kp);
+      vx[j] = *reinterpret_cast<const bf16x8*>(vp);
+    } else {
+      kx[j] = load_nt<bf16x8>(kp);
+      vx[j] = load_nt<bf16x8>(vp);
+    }
   }
   // owning sequence: the last b with qo_indptr[b] <= r
   int lo = 0, hi = a.B - 1;
