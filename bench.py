@@ -128,6 +128,33 @@ def cpu_oracle(w, tensors, budget_s: float, threads: int = HOST_THREADS) -> dict
     return res
 
 
+def calls_then_kernel(fn, kind: str, steps: int):
+    """Mean call time (ms) from HIP events around `steps` calls, then, in a second
+    pass with the library's kernel timer on, the number of timed launches and the
+    mean duration (ms) of the call's main kernel. The timer's events sit between
+    the kernels of a call, so they are kept out of the call timing."""
+    import torch
+
+    from paper_2609_08368_amd import rl_attn as ra
+
+    stream = torch.cuda.current_stream()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(steps):
+        fn()
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    ra.profile_read(kind)
+    ra.profile_enable(True)
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    ra.profile_enable(False)
+    n_k, kern_ms = ra.profile_read(kind)
+    return ms, n_k, kern_ms
+
+
 def timing_stats(v) -> dict:
     """Mean, median, min and 90th percentile of per-call times (ms)."""
     v = sorted(v)
@@ -452,18 +479,7 @@ def fp8_study(steps: int, warmup: int, w_dec, w_ext, bf16_dec_ms: float, bf16_ex
             fn()
         torch.cuda.synchronize()
         kind = "decode" if w.kind == "decode" else "extend"
-        ra.profile_read(kind)
-        ra.profile_enable(True)
-        stream = torch.cuda.current_stream()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for _ in range(steps):
-            fn()
-        b.record(stream)
-        torch.cuda.synchronize()
-        ra.profile_enable(False)
-        n_k, kern_ms = ra.profile_read(kind)
-        ms = a.elapsed_time(b) / steps
+        ms, n_k, kern_ms = calls_then_kernel(fn, kind, steps)
         fp8_bytes = w.kv_bytes() // 2          # one byte per element
         row = {"ms_mean": round(ms, 4), "kernel_ms": round(kern_ms, 4) if n_k else None,
                "speedup_vs_bf16": round((bf16_dec_ms if kind == "decode" else bf16_ext_ms) / ms, 3)}
@@ -546,18 +562,7 @@ def append_study(steps: int, warmup: int, w_ext, w_dec) -> dict:
             for _ in range(warmup):
                 fn()
             torch.cuda.synchronize()
-            stream = torch.cuda.current_stream()
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            ra.profile_read("append")
-            ra.profile_enable(True)
-            a.record(stream)
-            for _ in range(steps):
-                fn()
-            b.record(stream)
-            torch.cuda.synchronize()
-            ra.profile_enable(False)
-            _, kern_ms = ra.profile_read("append")
-            ms = a.elapsed_time(b) / steps
+            ms, _, kern_ms = calls_then_kernel(fn, "append", steps)
             elems = 2 * total * w.hkv * 128
             moved = elems * 2 + elems * (1 if fp8 else 2)        # read bf16 rows, write pages
             res[f"{wname}_{'fp8' if fp8 else 'bf16'}"] = {
@@ -591,18 +596,7 @@ def mtp_study(steps: int, warmup: int, w, t, single_ms: float) -> dict:
         for _ in range(warmup):
             fn()
         torch.cuda.synchronize()
-        ra.profile_read("decode")
-        ra.profile_enable(True)
-        stream = torch.cuda.current_stream()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for _ in range(steps):
-            fn()
-        b.record(stream)
-        torch.cuda.synchronize()
-        ra.profile_enable(False)
-        _, kern_ms = ra.profile_read("decode")
-        ms = a.elapsed_time(b) / steps
+        ms, _, kern_ms = calls_then_kernel(fn, "decode", steps)
         gbps = w.kv_bytes() / (ms * 1e-3) / 1e9
         res[f"n{n}"] = {"ms_mean": round(ms, 4), "kernel_ms": round(kern_ms, 4), "kv_GBps": round(gbps, 2),
                         "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
@@ -693,9 +687,6 @@ def main():
     stream = torch.cuda.current_stream()
     ev = {name: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                  for _ in range(args.steps)] for name, _ in parts}
-    ra.profile_read("decode")
-    ra.profile_read("extend")
-    ra.profile_enable(True)
     torch.cuda.synchronize()
     step_start = torch.cuda.Event(enable_timing=True)
     step_stop = torch.cuda.Event(enable_timing=True)
@@ -707,20 +698,26 @@ def main():
             ev[name][i][1].record(stream)
     step_stop.record(stream)
     torch.cuda.synchronize()
-    ra.profile_enable(False)
-    # kernel-level means: decode kernel launches alternate ragged / group (2 per step)
-    n_dec, dec_kernel_ms_all = ra.profile_read("decode")
-    n_ext, ext_kernel_ms = ra.profile_read("extend")
     total_ms = step_start.elapsed_time(step_stop)
     ms = {name: [a.elapsed_time(b) for a, b in ev[name]] for name in ev}
 
-    # separate kernel timing pass for the ragged decode alone (for the roofline)
+    # kernel-level timing in passes of their own, with the library's kernel
+    # timer on (its events would otherwise sit inside the timed calls): the
+    # ragged decode kernel (the roofline) and the extend kernel
+    ra.profile_read("decode")
     ra.profile_enable(True)
     for _ in range(args.steps):
         parts[0][1]()
     torch.cuda.synchronize()
     ra.profile_enable(False)
     n_k, dec_kernel_ms = ra.profile_read("decode")
+    ra.profile_read("extend")
+    ra.profile_enable(True)
+    for _ in range(args.steps):
+        extend()
+    torch.cuda.synchronize()
+    ra.profile_enable(False)
+    n_ext, ext_kernel_ms = ra.profile_read("extend")
 
     # the tiny and the uniform decode batches, timed call by call outside the step
     for name, t in (("decode_tiny", t_tiny), ("decode_uniform", t_uni)):
