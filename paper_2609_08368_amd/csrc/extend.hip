@@ -155,7 +155,7 @@ constexpr int kExtWaves = 8;            // waves per extend workgroup: 256 query
 // kernel, so the common case keeps its register allocation.
 constexpr int kStepPages = 0, kSetPages = 1, kRowPages = 2;
 
-template <bool kFp8, int kPages>
+template <bool kFp8, int kPages, bool kNt = false>
 __global__ __launch_bounds__(kExtWaves * 64, 2) void extend_mfma_kernel(ExtendArgs a) {
   __shared__ TileLds lds;
 
@@ -201,7 +201,7 @@ __global__ __launch_bounds__(kExtWaves * 64, 2) void extend_mfma_kernel(ExtendAr
   const bool active = __builtin_amdgcn_ballot_w64(row_ok) != 0;
   auto attend = [&](auto compute_tag) {
     constexpr bool kC = decltype(compute_tag)::value;
-    tile_attend_pp<kExtWaves, kPages != kRowPages, kFp8, kC, kPages == kSetPages>(
+    tile_attend_pp<kExtWaves, kPages != kRowPages, kFp8, kC, kPages == kSetPages, kNt>(
         a.kv, scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run, l_run, bad);
   };
   if (active)
@@ -233,9 +233,15 @@ hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream, KernelTimer* t
   const int64_t ss = a.kv.ss > a.kv.v_ss ? a.kv.ss : a.kv.v_ss;
   const bool scalar_ids = ((int64_t)a.kv.page_size * ss + kHeadDim) * 2 < (int64_t(1) << 31);
   const int pages = !scalar_ids ? kRowPages : (a.kv.page_size >= kKeys ? kStepPages : kSetPages);
+  // decode through the extend kernel with one unit per (sequence, KV head):
+  // every key row is read once, so the rows are loaded non-temporally (pages
+  // of at least a step only)
+  const bool once = a.decode_rows > 0 && a.head_blocks == 1 && a.decode_rows <= a.tile_tokens;
   auto go = [&](auto fp8_tag) {
     constexpr bool kF = decltype(fp8_tag)::value;
-    if (pages == kStepPages)
+    if (pages == kStepPages && once)
+      extend_mfma_kernel<kF, kStepPages, true><<<grid, kExtWaves * 64, 0, stream>>>(a);
+    else if (pages == kStepPages)
       extend_mfma_kernel<kF, kStepPages><<<grid, kExtWaves * 64, 0, stream>>>(a);
     else if (pages == kSetPages)
       extend_mfma_kernel<kF, kSetPages><<<grid, kExtWaves * 64, 0, stream>>>(a);

@@ -269,7 +269,8 @@ __device__ __forceinline__ void tile_attend(const PagedKV& kv, float scale, cons
 // in-page row offsets are fixed except for the clamp to the last key in the
 // sequence's final step, which stays in the page of its set. Otherwise every
 // thread looks up the page of each row it stages.
-template <int kWaves, bool kUniformPages, bool kFp8 = false, bool kCompute = true, bool kSetPages = false>
+template <int kWaves, bool kUniformPages, bool kFp8 = false, bool kCompute = true, bool kSetPages = false,
+          bool kNt = false>
 __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, const int* bt_row, int g, int t_lo,
                                                int t_hi, int t_full, int limit, const bf16x8 (&qv)[8], TileLds& lds,
                                                f32x16 (&o)[4], float& m_run, float& l_run, int& bad) {
@@ -312,6 +313,10 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
   const uint32_t ksp = (uint32_t)kv.sp, kss = (uint32_t)kv.ss;
   const uint32_t vsp = (uint32_t)kv.v_sp, vss = (uint32_t)kv.v_ss;
   const bool page_holds_step = kv.page_size >= kKeys;
+  // kNt: rows that no other work unit reads (decode through this routine)
+  // are loaded non-temporally; units that share keys through the L2 keep
+  // ordinary loads
+  auto load_row = [&](const char* p) { return kNt ? load_kv_raw_nt<kFp8>(p) : load_kv_raw<kFp8>(p); };
   auto load_ids = [&](int t0, Ids& ids) {
 #pragma unroll
     for (int i = 0; i < kStageRows; ++i) {
@@ -330,7 +335,7 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
         bad = 1;
         pg = pg < 0 ? 0 : kv.num_pages - 1;
       }
-      r[i] = load_kv_raw<kFp8>(base + ES * row_offset((uint32_t)pg, sp, t & pmask, ss));
+      r[i] = load_row(base + ES * row_offset((uint32_t)pg, sp, t & pmask, ss));
     }
   };
 
@@ -376,13 +381,13 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
     if (tc + kKeys <= t_hi) {
 #pragma unroll
       for (int i = 0; i < kStageRows; ++i)
-        r[i] = load_kv_raw<kFp8>(base + ES * ((int64_t)p[i] * sp) + step_off + off[i]);
+        r[i] = load_row(base + ES * ((int64_t)p[i] * sp) + step_off + off[i]);
     } else {
       const int last = t_hi - 1 - tc;
 #pragma unroll
       for (int i = 0; i < kStageRows; ++i) {
         const int rr = min(ld_row + kRowStep * i, last);
-        r[i] = load_kv_raw<kFp8>(base + ES * ((int64_t)p[i] * sp) +
+        r[i] = load_row(base + ES * ((int64_t)p[i] * sp) +
                                  ES * (ld_chunk + ((uint32_t)(tc + rr) & (uint32_t)pmask) * ss));
       }
     }
