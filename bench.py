@@ -583,25 +583,29 @@ def mtp_study(steps: int, warmup: int, w, t, single_ms: float) -> dict:
     from paper_2609_08368_amd import rl_attn as ra
 
     dev = torch.device("cuda:0")
-    res = {"workload": "ragged 64K decode batch, bf16 pages, n query tokens per sequence (the last n keys)"}
+    res = {"workload": "ragged 64K decode batch, bf16 pages, n query tokens per sequence (the last n keys)",
+           "prefix_share_off": {"note": "the same calls with prefix sharing off, which run through the extend "
+                                        "kernel (no split of the keys)"}}
     for n in (2, 4, 8):
         g = torch.Generator(device=dev)
         g.manual_seed(900 + n)
         q = torch.randn((w.batch, n, w.hq, 128), generator=g, device=dev).to(torch.bfloat16)
         out = torch.empty_like(q)
+        for share in (True, False):
+            def fn():
+                ra.decode(q, t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out,
+                          prefix_share=share)
 
-        def fn():
-            ra.decode(q, t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out)
-
-        for _ in range(warmup):
-            fn()
-        torch.cuda.synchronize()
-        ms, _, kern_ms = calls_then_kernel(fn, "decode", steps)
-        gbps = w.kv_bytes() / (ms * 1e-3) / 1e9
-        res[f"n{n}"] = {"ms_mean": round(ms, 4), "kernel_ms": round(kern_ms, 4), "kv_GBps": round(gbps, 2),
-                        "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
-                        "query_tokens_per_s": round(w.batch * n / (ms * 1e-3), 1),
-                        "time_vs_single_token": round(ms / single_ms, 3)}
+            for _ in range(warmup):
+                fn()
+            torch.cuda.synchronize()
+            ms, _, kern_ms = calls_then_kernel(fn, "decode", steps)
+            gbps = w.kv_bytes() / (ms * 1e-3) / 1e9
+            row = {"ms_mean": round(ms, 4), "kernel_ms": round(kern_ms, 4), "kv_GBps": round(gbps, 2),
+                   "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
+                   "query_tokens_per_s": round(w.batch * n / (ms * 1e-3), 1),
+                   "time_vs_single_token": round(ms / single_ms, 3)}
+            (res if share else res["prefix_share_off"])[f"n{n}"] = row
     log(f"multi-token decode: {res}")
     return res
 

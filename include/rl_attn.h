@@ -100,7 +100,12 @@ typedef struct {
                             0 = automatic, otherwise a multiple of 64
                             (RL_ERR_INVALID_ARG if not)                          */
   int32_t prefix_share;  /* enum rl_prefix_mode: read group-shared prefix pages once
-                            (AUTO) or treat every sequence independently (OFF)     */
+                            (AUTO) or treat every sequence independently (OFF).
+                            With OFF, automatic splits and more than one query
+                            token per sequence (q, out and lse with batch stride =
+                            tokens x token stride), decode runs as in the
+                            deterministic mode: faster when no pages are shared,
+                            and batch-invariant                                   */
   int32_t validate;      /* accepted for compatibility, no effect: every page id a
                             kernel reads is range-checked on every call           */
   int32_t deterministic; /* decode: 1 = batch-invariant and equal to extend. Each

@@ -111,6 +111,41 @@ def test_mtp_deterministic_equals_extend(n):
     check(w, t, n, out, lse, "mtp deterministic")
 
 
+@pytest.mark.parametrize("n", [2, 8])
+def test_mtp_unshared_runs_as_deterministic(n):
+    """With prefix sharing off and automatic splits, multi-token decode runs through
+    the extend kernel: bitwise the deterministic mode, and the oracle's values."""
+    w, t = mtp_problem(185 + n, [n, 333, 1500, 64 + n], n, 96, 8, 64)
+    H.say(f"mtp unshared n={n}")
+    out, lse = run_mtp(w, t, n, prefix_share=False)
+    do, dl = run_mtp(w, t, n, deterministic=True)
+    assert torch.equal(out.view(torch.int16), do.view(torch.int16)) and torch.equal(lse, dl)
+    check(w, t, n, out, lse, f"mtp unshared n={n}")
+    ra.check_device_errors()
+
+
+def test_mtp_unshared_split_path_cases():
+    """Prefix sharing off with a forced split, or with q rows that do not merge with the
+    batch dimension, keeps the split path (no error), and matches the oracle."""
+    n = 4
+    w, t = mtp_problem(190, [70, 900, 2100, 5], n, 96, 8, 64)
+    H.say("mtp unshared, forced split")
+    out, lse = run_mtp(w, t, n, prefix_share=False, split_tokens=256)
+    check(w, t, n, out, lse, "mtp unshared split 256")
+    H.say("mtp unshared, q with a padded batch stride")
+    B = w.batch
+    qpad = torch.zeros((B, n + 1, w.hq, 128), dtype=torch.bfloat16, device=DEV)
+    qpad[:, :n] = t["q"].view(B, n, w.hq, 128)
+    q = qpad[:, :n]                                   # batch stride (n + 1) x token stride
+    out = H.poison_like(torch.empty((B, n, w.hq, 128), dtype=torch.bfloat16, device=DEV))
+    lse = H.poison_like(torch.empty((B, n, w.hq), dtype=torch.float32, device=DEV))
+    ra.decode(q, t["k_pages"], t["v_pages"], t["block_table"], t["kv_lens"], t["scale"], out=out, lse=lse,
+              prefix_share=False)
+    torch.cuda.synchronize()
+    check(w, t, n, out, lse, "mtp unshared padded q")
+    ra.check_device_errors()
+
+
 def test_mtp_empty_sequence():
     w, t = mtp_problem(180, [0, 40, 0], 2, 8, 2, 16)
     H.say("mtp empty sequences")
