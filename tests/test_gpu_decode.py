@@ -36,6 +36,9 @@ CASES = [
     (16, 6, 3, [40, 1, 77], 64),             # GQA 2
     (16, 40, 2, [50, 190], 64),              # GQA 20: two 16-head blocks
     (64, 32, 1, [1000, 3], 256),
+    (32, 24, 2, [31, 32, 33, 97, 600], 0),   # pages of exactly one 32-key tile: whole-row loads
+    (32, 24, 2, [31, 32, 33, 97, 600], 64),
+    (16, 40, 2, [300, 17], 0),               # pages below a tile: each lane loads its share of a row
 ]
 
 

@@ -27,6 +27,8 @@ DECODE_CASES = [
     (32, 2, 2, [1, 31, 33, 250], 64),        # one query head per KV head: vector-ALU path
     (16, 40, 2, [50, 190], 64),              # two 16-head blocks
     (16, 8, 2, [0, 20, 0, 1], 0),            # empty sequences
+    (32, 24, 2, [31, 32, 33, 97, 600], 64),  # pages of exactly one 32-key tile: whole-row loads
+    (64, 96, 8, [5, 130, 257, 2000], 0),     # the agentic head shape
 ]
 
 
