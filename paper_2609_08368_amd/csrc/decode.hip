@@ -840,26 +840,44 @@ __global__ __launch_bounds__(64) void decode_valu_kernel(DecodeArgs a) {
   constexpr int ES = kv_bytes<kFp8>();
   const char* kbase = (const char*)a.kv.k + ES * ((int64_t)g * a.kv.sh + c16 * 8);
   const char* vbase = (const char*)a.kv.v + ES * ((int64_t)g * a.kv.v_sh + c16 * 8);
-  for (int t0 = t_begin; t0 < t_end; t0 += 4) {
-    const int t = t0 + grp;
-    const bool valid = t < t_end;
-    const int tt = valid ? t : t_end - 1;
-    const uint32_t pg = page_of(bt_row, bt_sj, tt, a.kv.log2_page, a.kv.num_pages, &bad);
-    const int slot_t = tt & (a.kv.page_size - 1);
-    const bf16x8 kk = load_kv8_nt<kFp8>(kbase + ES * row_offset(pg, (uint32_t)a.kv.sp, slot_t, (uint32_t)a.kv.ss));
-    const bf16x8 vv = load_kv8_nt<kFp8>(vbase + ES * row_offset(pg, (uint32_t)a.kv.v_sp, slot_t, (uint32_t)a.kv.v_ss));
-    float d = 0.f;
+  // kU keys per group per round (keys t0 + 4 u + grp): the round's page ids
+  // are loaded together, then its rows, so a round waits for two round trips
+  // instead of 2 kU; the keys are then taken in the same order as one at a time
+  constexpr int kU = 4;
+  for (int t0 = t_begin; t0 < t_end; t0 += 4 * kU) {
+    uint32_t pg[kU];
+    int slot_t[kU];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) d += qf[i] * (float)kk[i];
-    d = row_sum16(d);
-    if (valid) {
-      const float m_new = fmaxf(m, d);
-      const float alpha = exp2_fast(m - m_new);
-      const float p = exp2_fast(d - m_new);
-      l = l * alpha + p;
+    for (int u = 0; u < kU; ++u) {
+      const int t = t0 + 4 * u + grp;
+      const int tt = t < t_end ? t : t_end - 1;
+      pg[u] = page_of(bt_row, bt_sj, tt, a.kv.log2_page, a.kv.num_pages, &bad);
+      slot_t[u] = tt & (a.kv.page_size - 1);
+    }
+    KvRaw<kFp8> kr[kU], vr[kU];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) acc[i] = acc[i] * alpha + p * (float)vv[i];
-      m = m_new;
+    for (int u = 0; u < kU; ++u) {
+      kr[u] = load_kv_raw_nt<kFp8>(kbase + ES * row_offset(pg[u], (uint32_t)a.kv.sp, slot_t[u], (uint32_t)a.kv.ss));
+      vr[u] = load_kv_raw_nt<kFp8>(vbase + ES * row_offset(pg[u], (uint32_t)a.kv.v_sp, slot_t[u], (uint32_t)a.kv.v_ss));
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const bool valid = t0 + 4 * u + grp < t_end;
+      const bf16x8 kk = kv_to_bf16x8<kFp8>(kr[u]);
+      float d = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) d += qf[i] * (float)kk[i];
+      d = row_sum16(d);
+      if (valid) {
+        const bf16x8 vv = kv_to_bf16x8<kFp8>(vr[u]);
+        const float m_new = fmaxf(m, d);
+        const float alpha = exp2_fast(m - m_new);
+        const float p = exp2_fast(d - m_new);
+        l = l * alpha + p;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = acc[i] * alpha + p * (float)vv[i];
+        m = m_new;
+      }
     }
   }
   const float M = group_max(m);
