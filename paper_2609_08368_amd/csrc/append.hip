@@ -115,6 +115,16 @@ __global__ __launch_bounds__(kAppendThreads) void append_kernel(AppendArgs a) {
       vx[j] = load_nt<bf16x8>(vp);
     }
   }
+  // FP8: the heads' scales are read with the rows (one round trip for both)
+  float ksc[kGroup], vsc[kGroup];
+  if constexpr (kFp8) {
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j) {
+      const int g = g0 + (j < gn ? j : 0);
+      ksc[j] = a.k_scale[g * a.ks_s];
+      vsc[j] = a.v_scale[g * a.vs_s];
+    }
+  }
   // owning sequence: the last b with qo_indptr[b] <= r
   int lo = 0, hi = a.B - 1;
   while (lo < hi) {
@@ -152,7 +162,7 @@ __global__ __launch_bounds__(kAppendThreads) void append_kernel(AppendArgs a) {
       *reinterpret_cast<bf16x8*>((__bf16*)a.k + ko) = kx[j];
       *reinterpret_cast<bf16x8*>((__bf16*)a.v + vo) = vx[j];
     } else {
-      const float ks = a.k_scale[g * a.ks_s], vs = a.v_scale[g * a.vs_s];
+      const float ks = ksc[j], vs = vsc[j];
       if (!scale_ok(ks) || !scale_ok(vs)) {
         atomicOr(a.err, kErrScale);
         continue;
