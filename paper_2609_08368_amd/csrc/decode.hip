@@ -29,7 +29,7 @@ namespace rl {
 namespace {
 
 constexpr int kMinSplit = 256;     // smallest automatic split of shared keys
-constexpr int kMinWorkerKeys = 256; // fewest keys per private-pass worker (automatic)
+constexpr int kMinWorkerKeys = 64; // fewest keys per private-pass worker (automatic)
 constexpr int kTile = 32;          // keys per inner iteration of the private kernel
 constexpr int kGroupMax = 1024;    // batches up to this size get trajectory-group detection
 constexpr int kIntMax = 0x7fffffff;

@@ -25,7 +25,7 @@ from paper_2609_08368_amd import workloads as wl
 
 TILE = 32            # keys per private-pass tile
 MIN_SPLIT = 256      # smallest automatic split of shared keys
-MIN_WORKER_KEYS = 256
+MIN_WORKER_KEYS = 64
 GROUP_MAX = 1024     # batches up to this size get trajectory-group detection
 
 
