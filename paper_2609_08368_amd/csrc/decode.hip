@@ -542,7 +542,7 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
   const int worker = blockIdx.x / nch;
   const int wave = threadIdx.x >> 6;
   const int rem = (blockIdx.x - worker * nch) * wpg + wave;
-  // bf16 pages: a V tile and a K tile per wave; FP8 pages: a V tile
+  // the wave's V tile and K tile (K is staged only when a page holds a tile)
   VTile& vs = reinterpret_cast<VTile*>(vs_dyn)[2 * wave];
   VTile& ks = reinterpret_cast<VTile*>(vs_dyn)[2 * wave + 1];
   const int g = rem % a.Hkv;
