@@ -829,6 +829,7 @@ def main():
     result["ceilings"] = {
         "read_loop_GBps": round(read_gbps, 1), "read_loop_frac_of_spec": round(read_gbps / HBM_PEAK_GBPS, 4),
         "decode_over_read_loop": round(dec_gbps / read_gbps, 4),
+        "decode_kernel_over_read_loop": round(kern_gbps / read_gbps, 4),
         "mfma_bf16_loop_TFLOPs": round(loop_tflops, 1),
         "mfma_loop_frac_of_spec": round(loop_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
         "extend_frac_of_mfma_loop": round(ext_tflops / loop_tflops, 4),
