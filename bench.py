@@ -584,8 +584,11 @@ def mtp_study(steps: int, warmup: int, w, t, single_ms: float) -> dict:
 
     dev = torch.device("cuda:0")
     res = {"workload": "ragged 64K decode batch, bf16 pages, n query tokens per sequence (the last n keys)",
+           "route": "prefix sharing on: the decode planner finds no shared page in this batch, so the queued "
+                    "extend pass computes the rows (one unit per sequence and KV head) and the split passes "
+                    "return at once; kernel_ms spans every kernel of the call, planners included",
            "prefix_share_off": {"note": "the same calls with prefix sharing off, which run through the extend "
-                                        "kernel (no split of the keys)"}}
+                                        "kernel directly (no split of the keys, no decode planner)"}}
     for n in (2, 4, 8):
         g = torch.Generator(device=dev)
         g.manual_seed(900 + n)

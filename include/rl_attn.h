@@ -101,11 +101,15 @@ typedef struct {
                             (RL_ERR_INVALID_ARG if not)                          */
   int32_t prefix_share;  /* enum rl_prefix_mode: read group-shared prefix pages once
                             (AUTO) or treat every sequence independently (OFF).
-                            With OFF, automatic splits and more than one query
-                            token per sequence (q, out and lse with batch stride =
+                            With automatic splits and more than one query token
+                            per sequence (q, out and lse with batch stride =
                             tokens x token stride), decode runs as in the
-                            deterministic mode: faster when no pages are shared,
-                            and batch-invariant                                   */
+                            deterministic mode (one extend unit per sequence and
+                            KV head, no split of the keys; faster when no pages
+                            are shared, and batch-invariant): with OFF always;
+                            with AUTO and bf16 pages when the device finds no
+                            shared prefix page in the batch (both passes are
+                            queued, the one not needed does no work)            */
   int32_t validate;      /* accepted for compatibility, no effect: every page id a
                             kernel reads is range-checked on every call           */
   int32_t deterministic; /* decode: 1 = batch-invariant and equal to extend. Each

@@ -359,6 +359,11 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
   // workers whose share starts before tile y of the concatenation (0 < y <= W)
   auto starts_before = [&](long long y) -> long long { return (y * nwork + W - 1) / W; };
 
+  // Multi-token decode with no shared prefix page and an extend pass queued
+  // behind this one: that pass computes every row (one unit per sequence and
+  // KV head, longest first), and the split passes get no work.
+  const bool handoff = a.route_extend && n_sg == 0;
+
   // Per sequence: its shared splits (level by level), then one private piece
   // per worker share it overlaps (a worker start strictly inside the range
   // begins a new piece)
@@ -384,8 +389,8 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
       // a sequence whose slots do not fit writes nothing (the host sizes the
       // workspace so that this never happens; it is reported, not raced)
       const bool fits = slot_base + nslots <= a.max_slots;
-      if (!fits) cap_bad = 1;
-      a.ws.nparts[b] = empty ? -1 : (fits ? nslots : -2);
+      if (!fits && !handoff) cap_bad = 1;
+      a.ws.nparts[b] = handoff ? 0 : (empty ? -1 : (fits ? nslots : -2));
       a.ws.base[b] = slot_base;
       a.ws.seqs[b] = make_int4(S, !fits ? kSlotDropped : (direct ? kSlotDirect : slot_base + nsh), L, fits ? 1 : 0);
       // its place in the sub-groups of every node it belongs to; a node's
@@ -430,7 +435,7 @@ __global__ __launch_bounds__(1024) void plan_decode_kernel(DecodeArgs a) {
   }
   if (tid == 0) {
     a.ws.hdr[0] = C;
-    a.ws.hdr[1] = nwork;
+    a.ws.hdr[1] = handoff ? 0 : nwork;
     a.ws.hdr[2] = min(sitem_off, a.max_items);
     a.ws.hdr[3] = n_sg;
   }
@@ -1124,15 +1129,22 @@ __device__ __forceinline__ void merge_parts(const float* o_base, int64_t o_step,
   *lse_out = z > 0.f ? M + __builtin_amdgcn_logf(z) * kLn2 : kNegInf;
 }
 
-__global__ __launch_bounds__(64) void combine_kernel(DecodeArgs a) {
-  // one (sequence, row) per wave; row hv = token * Hq + query head
-  const int b = blockIdx.x / a.Hv;
-  const int hv = blockIdx.x - b * a.Hv;
-  const int tok = hv / a.Hq, h = hv - tok * a.Hq;
+// One (sequence, row) per wave, kCombineRows rows of one sequence per
+// workgroup (row hv = token * Hq + query head): a sequence without parts to
+// merge costs one workgroup per kCombineRows rows rather than one per row
+// (at 8 tokens of 96 heads, 98K single-wave workgroups took 25 us to launch
+// and return).
+constexpr int kCombineRows = 8;
+
+__global__ __launch_bounds__(kCombineRows * 64) void combine_kernel(DecodeArgs a) {
+  const int nblk = (a.Hv + kCombineRows - 1) / kCombineRows;
+  const int b = blockIdx.x / nblk;
+  const int hv = (blockIdx.x - b * nblk) * kCombineRows + (threadIdx.x >> 6);
   // the planner writes both for every sequence; they are read together
   const int n = a.ws.nparts[b];
   const int base = a.ws.base[b];
-  if (n == 0) return;     // written directly by its only piece
+  if (n == 0 || hv >= a.Hv) return;     // n == 0: written directly by its only piece
+  const int tok = hv / a.Hq, h = hv - tok * a.Hq;
   float r[2] = {0.f, 0.f}, lse_v = kNegInf;   // an empty sequence (n == -1): zeros, -inf
   if (n == -2) {          // its slots did not fit the workspace (reported as kErrCapacity)
     r[0] = r[1] = lse_v = __uint_as_float(0x7fc00000u);   // a quiet NaN
@@ -1140,7 +1152,7 @@ __global__ __launch_bounds__(64) void combine_kernel(DecodeArgs a) {
     merge_parts(a.ws.part_o + ((int64_t)base * a.Hv + hv) * kHeadDim, (int64_t)a.Hv * kHeadDim,
                 a.ws.part_lse + (int64_t)base * a.Hv + hv, a.Hv, n, r, &lse_v);
   }
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;
   const int64_t oo = (int64_t)b * a.out_sb + (int64_t)tok * a.out_st + (int64_t)h * a.out_sh + 2 * lane;
   if (a.out_f32) {
     float* op = (float*)a.out + oo;
@@ -1220,7 +1232,8 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream, KernelTimer* t
     launch_decode_kernels<true>(a, stream, timer);
   else
     launch_decode_kernels<false>(a, stream, timer);
-  combine_kernel<<<(unsigned)((int64_t)a.B * a.Hv), 64, 0, stream>>>(a);
+  combine_kernel<<<(unsigned)((int64_t)a.B * ((a.Hv + kCombineRows - 1) / kCombineRows)), kCombineRows * 64, 0,
+                   stream>>>(a);
   return hipGetLastError();
 }
 

@@ -70,23 +70,39 @@ __global__ __launch_bounds__(1024) void plan_extend_kernel(ExtendArgs a) {
   __shared__ int wave_tot[16];
   const int tid = threadIdx.x;
   int bad = 0;
+  if (a.gate && *a.gate != 0) {          // the split decode passes compute the rows
+    if (tid == 0) a.ws.hdr[0] = 0;
+    return;
+  }
   if (a.decode_rows) {
-    // decode rows of empty sequences have no work unit: out = 0, lse = -inf
+    // decode rows of empty sequences have no work unit: out = 0, lse = -inf.
+    // The empty sequences of each pass of blockDim sequences are listed first
+    // (one length load per thread), then their rows are written by all threads.
+    __shared__ int empties[1024];
+    __shared__ int n_empty;
     const int per_seq = a.decode_rows * a.Hq;
-    for (int i = tid; i < a.B * per_seq; i += blockDim.x) {
-      const int b = i / per_seq, rest = i - b * per_seq;
-      const int64_t row = (int64_t)b * a.decode_rows + rest / a.Hq;
-      const int h = rest % a.Hq;
+    for (int b0 = 0; b0 < a.B; b0 += blockDim.x) {
+      if (tid == 0) n_empty = 0;
+      __syncthreads();
+      const int b = b0 + tid;
       int dummy = 0;
-      if (seq_range(a, b, &dummy).n != 0) continue;
-      if (a.out_f32) {
-        float4* op = reinterpret_cast<float4*>((float*)a.out + row * a.out_st + (int64_t)h * a.out_sh);
-        for (int c = 0; c < kHeadDim / 4; ++c) op[c] = make_float4(0.f, 0.f, 0.f, 0.f);
-      } else {
-        uint4* op = reinterpret_cast<uint4*>((__bf16*)a.out + row * a.out_st + (int64_t)h * a.out_sh);
-        for (int c = 0; c < kHeadDim / 8; ++c) op[c] = make_uint4(0u, 0u, 0u, 0u);
+      if (b < a.B && seq_range(a, b, &dummy).n == 0) empties[atomicAdd(&n_empty, 1)] = b;
+      __syncthreads();
+      const int rows = n_empty * per_seq;
+      for (int i = tid; i < rows; i += blockDim.x) {
+        const int e = empties[i / per_seq], rest = i % per_seq;
+        const int64_t row = (int64_t)e * a.decode_rows + rest / a.Hq;
+        const int h = rest % a.Hq;
+        if (a.out_f32) {
+          float4* op = reinterpret_cast<float4*>((float*)a.out + row * a.out_st + (int64_t)h * a.out_sh);
+          for (int c = 0; c < kHeadDim / 4; ++c) op[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+        } else {
+          uint4* op = reinterpret_cast<uint4*>((__bf16*)a.out + row * a.out_st + (int64_t)h * a.out_sh);
+          for (int c = 0; c < kHeadDim / 8; ++c) op[c] = make_uint4(0u, 0u, 0u, 0u);
+        }
+        if (a.lse) a.lse[row * a.lse_st + (int64_t)h * a.lse_sh] = kNegInf;
       }
-      if (a.lse) a.lse[row * a.lse_st + (int64_t)h * a.lse_sh] = kNegInf;
+      __syncthreads();                   // the list is rebuilt for the next pass
     }
   }
   const bool sorted = a.B <= kSortMax;

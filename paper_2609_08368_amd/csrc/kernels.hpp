@@ -100,6 +100,11 @@ struct DecodeArgs {
   int group_cap;          // members per sub-group (128 query rows / (n_tok * R)), 0 = no prefix sharing
   int prefix_grid;        // workgroups of the group-prefix pass (grid-stride over its work)
   int item_waves;         // waves per decode workgroup: a divisor of Hkv * ceil(R / 16), at most 8
+  // multi-token decode with an extend pass queued behind it: when the planner
+  // finds no shared prefix page, the split passes get no work (no workers, no
+  // parts to combine) and the extend pass, gated on the sub-group count in
+  // ws.hdr[3], computes every row
+  int route_extend;
   DecodePlanWs ws;
 };
 
@@ -132,6 +137,10 @@ struct ExtendArgs {
   // not read), and the rows of empty sequences are written as zeros with
   // lse = -inf
   int decode_rows;
+  // nullable: the extend planner queues no unit (and writes nothing) when
+  // *gate != 0, i.e. when the decode planner that runs before it found shared
+  // prefix pages and the split passes compute the rows
+  const int* gate;
   ExtendPlanWs ws;
 };
 

@@ -530,12 +530,18 @@ size_t extend_ws_bytes(int64_t B, int64_t total_q, int64_t Hkv, int64_t R, int* 
 
 // Work-unit shape, workspace and launch of an extend call whose arguments
 // (pages, q, lengths, output) are already filled in. prof_kind: which timing
-// slot the attention kernel is counted under.
-int run_extend(rl::ExtendArgs& a, hipStream_t st, int prof_kind, bool noalloc = false) {
+// slot the attention kernel is counted under; `given`: a workspace already
+// carved out of the call's (else the stream's is taken); `timed`: whether the
+// kernel timer is recorded around the launch.
+int run_extend(rl::ExtendArgs& a, hipStream_t st, int prof_kind, bool noalloc = false, const WsView* given = nullptr,
+               bool timed = true) {
   int max_items = 0;
   const size_t bytes = extend_ws_bytes(a.B, a.total_q, a.Hkv, a.R, &max_items);
   WsView w{};
-  RL_TRY(get_ws(st, bytes, noalloc, &w));
+  if (given)
+    w = *given;
+  else
+    RL_TRY(get_ws(st, bytes, noalloc, &w));
   char* base = w.ptr;
   const ExtendShape s = extend_shape(a.R);
   a.rows_head = s.rows_head;
@@ -546,7 +552,7 @@ int run_extend(rl::ExtendArgs& a, hipStream_t st, int prof_kind, bool noalloc = 
   a.ws.items = reinterpret_cast<int4*>(base + 256);
   a.ws.err = w.err;
   rl::KernelTimer slot;
-  rl::KernelTimer* timer = noalloc ? nullptr : prof_timer(&slot, st);
+  rl::KernelTimer* timer = noalloc || !timed ? nullptr : prof_timer(&slot, st);
   hipError_t e = rl::launch_extend(a, st, timer);
   prof_commit(prof_kind, timer);
   if (e != hipSuccess) return hip_fail(e, "extend kernel launch");
@@ -597,12 +603,42 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   // merge with the batch dimension
   const bool rows_merge = !multi || (q->strides[0] == n_tok * q_st && out->strides[0] == n_tok * out_st &&
                                      (!lse_out || lse_out->strides[0] == n_tok * lse_st));
-  // Multi-token decode with prefix sharing off and automatic splits also runs
-  // through the extend kernel: one unit per (sequence, KV head) reads every
-  // key once, measured faster than the split path on the ragged 64K batch
-  // (n = 2, 4, 8: 1.57, 1.69, 1.90 against 1.72, 1.81, 1.95 ms per call).
-  // With sharing on the split path stays, since it reads group-shared pages
-  // once per group.
+  // Multi-token decode of a batch without shared prefix pages runs through the
+  // extend kernel: one unit per (sequence, KV head), longest first, reads every
+  // key once with no split and no combine, measured faster than the split path
+  // on the ragged 64K batch (n = 2, 4, 8: 1.57, 1.69, 1.90 against 1.72, 1.81,
+  // 1.95 ms per call; the split path through the extend kernel's tile routine
+  // was no faster, so the difference is the schedule). With prefix sharing off
+  // the host takes that route; with sharing on (automatic splits, bf16 pages)
+  // both passes are queued and the device decides: the decode planner finds
+  // the shared nodes, and with none it gives the split passes no work and the
+  // extend planner, gated on its sub-group count, lays out the units. FP8
+  // pages keep the split path (n = 4: 1.43 against 1.62 ms through extend).
+  auto extend_rows = [&]() {
+    rl::ExtendArgs x{};
+    x.kv = a.kv;
+    x.q = q->data;
+    x.q_st = multi ? q_st : q->strides[0];
+    x.q_sh = q->strides[hd];
+    x.qo_indptr = nullptr;
+    x.kv_lens = static_cast<const int*>(seq_lens->data);
+    x.kv_lens_s = seq_lens->strides[0];
+    x.B = (int)B;
+    x.total_q = (int)(B * n_tok);
+    x.Hq = (int)Hq;
+    x.Hkv = (int)Hkv;
+    x.R = (int)(Hq / Hkv);
+    x.scale = scale;
+    x.out = out->data;
+    x.out_f32 = is_f32;
+    x.out_st = multi ? out_st : out->strides[0];
+    x.out_sh = out->strides[hd];
+    x.lse = lse_out ? static_cast<float*>(lse_out->data) : nullptr;
+    x.lse_st = lse_out ? (multi ? lse_st : lse_out->strides[0]) : 0;
+    x.lse_sh = lse_out ? lse_out->strides[multi ? 2 : 1] : 0;
+    x.decode_rows = (int)n_tok;
+    return x;
+  };
   const bool via_extend =
       o.deterministic || (n_tok > 1 && o.prefix_share == RL_PREFIX_OFF && o.split_tokens == 0 && rows_merge);
   if (via_extend) {
@@ -613,29 +649,8 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
     if (!rows_merge)
       return fail(RL_ERR_UNSUPPORTED,
                   "deterministic multi-token decode needs q, out and lse_out with batch stride = tokens x token stride");
-    rl::ExtendArgs e{};
-    e.kv = a.kv;
-    e.q = q->data;
-    e.q_st = multi ? q_st : q->strides[0];
-    e.q_sh = q->strides[hd];
-    e.qo_indptr = nullptr;
-    e.kv_lens = static_cast<const int*>(seq_lens->data);
-    e.kv_lens_s = seq_lens->strides[0];
-    e.B = (int)B;
-    e.total_q = (int)(B * n_tok);
-    e.Hq = (int)Hq;
-    e.Hkv = (int)Hkv;
-    e.R = (int)(Hq / Hkv);
-    e.scale = scale;
-    e.out = out->data;
-    e.out_f32 = is_f32;
-    e.out_st = multi ? out_st : out->strides[0];
-    e.out_sh = out->strides[hd];
-    e.lse = lse_out ? static_cast<float*>(lse_out->data) : nullptr;
-    e.lse_st = lse_out ? (multi ? lse_st : lse_out->strides[0]) : 0;
-    e.lse_sh = lse_out ? lse_out->strides[multi ? 2 : 1] : 0;
-    e.decode_rows = (int)n_tok;
-    return run_extend(e, st, 0, noalloc);
+    rl::ExtendArgs x = extend_rows();
+    return run_extend(x, st, 0, noalloc);
   }
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -643,8 +658,23 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   const int cus = device_cus(dev);
   const DecodeLayout lay = decode_layout(B, Hq, Hkv, a.kv.max_pages, a.kv.page_size, o.split_tokens, cus,
                                          o.prefix_share == RL_PREFIX_AUTO, kv_dtype == RL_FP8_E4M3, (int)n_tok);
+  // the extend pass's work list follows the decode workspace; the
+  // allocation-free entry point keeps the split path alone when both do not
+  // fit its static array
+  bool route = n_tok > 1 && o.prefix_share == RL_PREFIX_AUTO && o.split_tokens == 0 && rows_merge &&
+               kv_dtype != RL_FP8_E4M3;
+  const size_t ext_off = align256(lay.total);
+  int ext_items = 0;
+  size_t need = lay.total;
+  if (route) {
+    need = ext_off + extend_ws_bytes(B, B * n_tok, Hkv, Hq / Hkv, &ext_items);
+    if (noalloc && need > rl::kScratchBytes - rl::kScratchErrBytes) {
+      route = false;
+      need = lay.total;
+    }
+  }
   WsView w{};
-  RL_TRY(get_ws(st, lay.total, noalloc, &w));
+  RL_TRY(get_ws(st, need, noalloc, &w));
   char* base = w.ptr;
   a.q = q->data;
   a.q_sb = q->strides[0];
@@ -688,12 +718,30 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   a.ws.part_o = reinterpret_cast<float*>(base + lay.off_po);
   a.ws.part_lse = reinterpret_cast<float*>(base + lay.off_pl);
   a.ws.err = w.err;
+  a.route_extend = route ? 1 : 0;
   rl::KernelTimer slot;
   rl::KernelTimer* timer = noalloc ? nullptr : prof_timer(&slot, st);
-  e = rl::launch_decode(a, st, timer);
+  if (!route) {
+    e = rl::launch_decode(a, st, timer);
+    prof_commit(0, timer);
+    if (e != hipSuccess) return hip_fail(e, "decode kernel launch");
+    return RL_OK;
+  }
+  // both passes: the timer spans them, planners included (either the split
+  // passes or the extend pass does the work)
+  if (timer) (void)hipEventRecord(timer->start, st);
+  e = rl::launch_decode(a, st, nullptr);
+  int rc = RL_OK;
+  if (e == hipSuccess) {
+    rl::ExtendArgs x = extend_rows();
+    x.gate = a.ws.hdr + 3;
+    const WsView xw{base + ext_off, w.err};
+    rc = run_extend(x, st, 0, noalloc, &xw, false);
+  }
+  if (timer) (void)hipEventRecord(timer->stop, st);
   prof_commit(0, timer);
   if (e != hipSuccess) return hip_fail(e, "decode kernel launch");
-  return RL_OK;
+  return rc;
 }
 
 int extend_impl(const rl_tensor* q, const rl_tensor* qo_indptr, const rl_tensor* k_pages, const rl_tensor* v_pages,
@@ -1012,15 +1060,20 @@ size_t rl_attn_decode_workspace_size(int64_t batch, int64_t num_q_heads, int64_t
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) == hipSuccess) cus = device_cus(dev);
   const int split = split_tokens ? split_tokens : env().split_tokens;
-  // bf16 and FP8 pages may keep different numbers of workers resident, and a
-  // deterministic decode uses the extend work list: the largest of the three
+  // bf16 and FP8 pages may keep different numbers of workers resident, a
+  // deterministic decode uses the extend work list, and a multi-token decode
+  // with prefix sharing on queues both (the extend list after the decode
+  // workspace): the largest of these
   int mi = 0;
   const int64_t R = num_q_heads / num_kv_heads;
-  size_t total = R >= 1 ? extend_ws_bytes(batch, batch * query_tokens, num_kv_heads, R, &mi) : 0;
-  for (bool fp8 : {false, true})
-    total = std::max(total, decode_layout(batch, num_q_heads, num_kv_heads, max_pages, page_size, split, cus,
-                                          true, fp8, (int)query_tokens)
-                                .total);
+  const size_t ext = R >= 1 ? extend_ws_bytes(batch, batch * query_tokens, num_kv_heads, R, &mi) : 0;
+  size_t total = ext;
+  for (bool fp8 : {false, true}) {
+    const size_t dec = decode_layout(batch, num_q_heads, num_kv_heads, max_pages, page_size, split, cus, true, fp8,
+                                     (int)query_tokens)
+                           .total;
+    total = std::max(total, query_tokens > 1 ? align256(dec) + ext : dec);
+  }
   return total;
 }
 

@@ -146,6 +146,28 @@ def test_mtp_unshared_split_path_cases():
     ra.check_device_errors()
 
 
+@pytest.mark.parametrize("n", [2, 8])
+def test_mtp_route_follows_shared_pages(n):
+    """Prefix sharing on, bf16 pages, automatic splits: a batch without shared pages is
+    computed by the queued extend pass (bitwise the deterministic mode); a trajectory-group
+    batch by the split passes, whose rows the extend pass must leave alone."""
+    w, t = mtp_problem(190 + n, [n, 300, 1400, 64 + n], n, 96, 8, 64)
+    H.say(f"mtp route without shared pages n={n}")
+    out, lse = run_mtp(w, t, n)
+    do, dl = run_mtp(w, t, n, deterministic=True)
+    assert torch.equal(out.view(torch.int16), do.view(torch.int16)) and torch.equal(lse, dl)
+    check(w, t, n, out, lse, f"mtp route no sharing n={n}")
+    gs, shared = 4, 1024
+    lens = [shared + 64 + 37 * j + 5 * g for g in range(2) for j in range(gs)]
+    w, t = mtp_problem(195 + n, lens, 2, 16, 4, 64, group_size=gs, shared_tokens=shared)
+    H.say("mtp route with shared pages n=2")
+    out, lse = run_mtp(w, t, 2)
+    do, dl = run_mtp(w, t, 2, deterministic=True)
+    assert not torch.equal(lse, dl), "the extend pass overwrote the split passes' rows"
+    check(w, t, 2, out, lse, "mtp route sharing")
+    ra.check_device_errors()
+
+
 def test_mtp_empty_sequence():
     w, t = mtp_problem(180, [0, 40, 0], 2, 8, 2, 16)
     H.say("mtp empty sequences")
