@@ -258,3 +258,19 @@ def test_capacity_model_reaches_its_bounds():
     caps["hkv"] = 8
     items_t, _, _ = plan_decode([int(x) for x in w.kv_lens], w.block_table, 64, caps, 0)
     assert items_t >= 16 + 32 + 64       # at least one split per node of each level
+
+
+def align256(x):
+    return (x + 255) // 256 * 256
+
+
+@pytest.mark.parametrize("n_tok", [2, 4, 8, 64])
+def test_multi_token_workspace_covers_both_passes(n_tok):
+    """With prefix sharing on, a multi-token decode call queues the split passes and an
+    extend pass, and carves the extend work list after the decode workspace: the size
+    query (what a caller reserves before capturing a graph) covers both."""
+    for B, hq, hkv, max_pages, P in ((128, 96, 8, 1024, 64), (3, 8, 2, 40, 16), (1000, 64, 8, 64, 64)):
+        dec = ra.diag_decode_capacity(B, hq, hkv, max_pages, P, n_tok, 0, True, 256, 1)["bytes"]
+        ext = ra.diag_extend_capacity(B, B * n_tok, hq, hkv)
+        need = align256(dec) + 256 + align256(ext["max_items"] * 16)
+        assert ra.decode_workspace_size(B, hq, hkv, max_pages, P, query_tokens=n_tok) >= need
