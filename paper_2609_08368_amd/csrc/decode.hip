@@ -18,7 +18,9 @@
 // A sequence whose whole context is one private item writes its output
 // directly; otherwise every item writes an (o, lse) partial into a slot of the
 // sequence and the combine kernel merges them (flash-decoding; the merge is the
-// log-sum-exp identity).
+// log-sum-exp identity). A multi-token call may queue an extend pass behind
+// these (route_extend): when the planner finds no shared prefix page it hands
+// every row to that pass and gives the split passes no work.
 #include <type_traits>
 
 #include "kernels.hpp"

@@ -52,7 +52,8 @@ constexpr int kPrefixLevels = 3;
 // 128 query rows). Partial results
 // live in "slots"; sequence b owns slots base[b] .. base[b] + nparts[b] - 1:
 // its shared splits, then its private pieces in key order (nparts[b] == 0:
-// one piece, written directly; -1: an empty sequence, written by the combine;
+// one piece, written directly, or every row left to the extend pass a
+// multi-token call queued; -1: an empty sequence, written by the combine;
 // -2: its slots did not fit, so the combine writes NaN and the error word
 // records kErrCapacity).
 struct DecodePlanWs {
