@@ -188,7 +188,8 @@ def pmc_workload(kind: str = "ragged"):
 
     ragged: three ragged-64K decode calls, then three copies of CALIB_BYTES (the
     calibration kernel for FETCH_SIZE / WRITE_SIZE); ragged-fp8: the same with FP8
-    E4M3 pages; ragged-mtp4: the same pages with 4 query tokens per sequence;
+    E4M3 pages; ragged-mtp2 / -mtp4 / -mtp8: the same pages with 2, 4 or 8 query tokens
+    per sequence;
     extend: two multi-turn extend calls; group / group-noshare: three decode calls
     of the 16x8 trajectory-group batch with prefix sharing on / off, then the same
     calibration copies; branch / branch-noshare: the same for the 16x8 branching
@@ -199,9 +200,10 @@ def pmc_workload(kind: str = "ragged"):
     from paper_2609_08368_amd import workloads as wl
 
     dev = torch.device("cuda:0")
-    w = {"ragged": wl.decode_ragged, "ragged-fp8": wl.decode_ragged, "ragged-mtp4": wl.decode_ragged,
-         "extend": wl.extend_multiturn, "branch": wl.decode_branching,
-         "branch-noshare": wl.decode_branching}.get(kind, wl.decode_group_prefix)()
+    mtp = int(kind[len("ragged-mtp"):]) if kind.startswith("ragged-mtp") else 0
+    w = {"ragged": wl.decode_ragged, "ragged-fp8": wl.decode_ragged, "extend": wl.extend_multiturn,
+         "branch": wl.decode_branching, "branch-noshare": wl.decode_branching}.get(
+             "ragged" if mtp else kind, wl.decode_group_prefix)()
     fp8 = kind == "ragged-fp8"
     t = (wl.materialize_fp8 if fp8 else wl.materialize)(w, dev, poison=False)
     out = torch.empty_like(t["q"])
@@ -225,10 +227,10 @@ def pmc_workload(kind: str = "ragged"):
                           "calib_bytes": CALIB_BYTES}), flush=True)
         return
     share = {"prefix_share": not kind.endswith("-noshare")}
-    if kind == "ragged-mtp4":
+    if mtp:
         g = torch.Generator(device=dev)
-        g.manual_seed(904)
-        t["q"] = torch.randn((w.batch, 4, w.hq, 128), generator=g, device=dev).to(torch.bfloat16)
+        g.manual_seed(900 + mtp)
+        t["q"] = torch.randn((w.batch, mtp, w.hq, 128), generator=g, device=dev).to(torch.bfloat16)
         out = torch.empty_like(t["q"])
     for _ in range(3):
         if fp8:
@@ -622,8 +624,8 @@ def main():
                     help="scales the oracle baseline's wall-time budgets (15: 33 s over the five workloads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pmc-workload", nargs="?", const="ragged",
-                    choices=["ragged", "ragged-fp8", "ragged-mtp4", "extend", "group", "group-noshare", "branch",
-                             "branch-noshare"],
+                    choices=["ragged", "ragged-fp8", "ragged-mtp2", "ragged-mtp4", "ragged-mtp8", "extend", "group",
+                             "group-noshare", "branch", "branch-noshare"],
                     help="run only what a counter run profiles")
     ap.add_argument("--summarize-counters", metavar="PMC_DIR", help="per-kernel means of a rocprofv3 --pmc run")
     ap.add_argument("--prefix-study", action="store_true", help="time group-prefix decode with sharing on and off")
