@@ -749,13 +749,29 @@ __global__ __launch_bounds__(512) void decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) o[j] *= alpha;
       __syncthreads();  // V tile visible
+      // V^T operand: element e of lane (grp, col) is V[tok(e)][16 j + col], tok(e) =
+      // 4 grp + e (e < 4) or 16 + 4 grp + e - 4 (the keys of pb). With FP8 pages
+      // two transposed reads per MFMA give it: lane 4e + q of a 16-lane block
+      // addresses row 4 grp + e (then 16 rows further), columns 16 j + 4 q ..
+      // + 3, and the read hands lane i element i % 4 of lane 4e + i / 4's chunk
+      // as its element e (FP8 decode 0.834 -> 0.816 ms on the ragged batch).
+      // bf16 keeps eight 16-bit reads: the transposed form measured 0.5-0.9%
+      // slower there, its registers allocated differently.
+      const int tr_row = 4 * grp + ((lane & 15) >> 2), tr_col = 4 * (lane & 3);
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         bf16x8 va;
+        if constexpr (kFp8) {
+          const u16* vp = &vs[tr_row][16 * j + tr_col];
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)vp);
+          const i16x4 up = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vp + 16 * (kHeadDim + 8)));
+          va = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
+        } else {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int tok = e < 4 ? 4 * grp + e : 16 + 4 * grp + (e - 4);
-          va[e] = bits_to_bf16(vs[tok][16 * j + col]);
+          for (int e = 0; e < 8; ++e) {
+            const int tok = e < 4 ? 4 * grp + e : 16 + 4 * grp + (e - 4);
+            va[e] = bits_to_bf16(vs[tok][16 * j + col]);
+          }
         }
         o[j] = mfma_16x16x32(va, pb, o[j]);
       }
