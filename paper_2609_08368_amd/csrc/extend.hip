@@ -168,13 +168,13 @@ constexpr int kExtWaves = 8;            // waves per extend workgroup: 256 query
 // Page lookups of the tile routine, chosen on the host: one scalar id per
 // step (pages of at least 64 keys), one per wave and 32-row set (smaller
 // pages), or one per row (in-page offsets past 31 bits). Each is its own
-// kernel, so the common case keeps its register allocation.
-constexpr int kStepPages = 0, kSetPages = 1, kRowPages = 2;
+// kernel, so the common case keeps its register allocation. bf16 pages of at
+// least 64 keys take 128-key steps with rows loaded straight into LDS
+// (kDirectPages).
+constexpr int kStepPages = 0, kSetPages = 1, kRowPages = 2, kDirectPages = 3;
 
 template <bool kFp8, int kPages, bool kNt = false>
 __global__ __launch_bounds__(kExtWaves * 64, 2) void extend_mfma_kernel(ExtendArgs a) {
-  __shared__ TileLds lds;
-
   // Units run in list order (longest key range first). Workgroups are handed
   // to the XCDs round-robin, so each XCD takes every eighth entry; the planner
   // lays the list out so those are the units of the (sequence, KV head) groups
@@ -215,15 +215,27 @@ __global__ __launch_bounds__(kExtWaves * 64, 2) void extend_mfma_kernel(ExtendAr
   // a wave whose 32 rows are all past the unit's tokens (a short chunk, or
   // the one token of a deterministic decode) only stages
   const bool active = __builtin_amdgcn_ballot_w64(row_ok) != 0;
-  auto attend = [&](auto compute_tag) {
-    constexpr bool kC = decltype(compute_tag)::value;
-    tile_attend_pp<kExtWaves, kPages != kRowPages, kFp8, kC, kPages == kSetPages, kNt>(
-        a.kv, scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run, l_run, bad);
-  };
-  if (active)
-    attend(std::true_type{});
-  else
-    attend(std::false_type{});
+  if constexpr (kPages == kDirectPages) {
+    static_assert(!kFp8, "rows go to LDS as stored: bf16 pages only");
+    __shared__ __attribute__((aligned(16))) char kl0[kDlKBytes], kl1[kDlKBytes], vl0[kDlVBytes], vl1[kDlVBytes];
+    if (active)
+      tile_attend_dl<true, kNt>(a.kv, scale, bt_row, g, t_end, t_full, limit, qv, kl0, kl1, vl0, vl1, o, m_run,
+                                l_run, bad);
+    else
+      tile_attend_dl<false, kNt>(a.kv, scale, bt_row, g, t_end, t_full, limit, qv, kl0, kl1, vl0, vl1, o, m_run,
+                                 l_run, bad);
+  } else {
+    __shared__ TileLds lds;
+    auto attend = [&](auto compute_tag) {
+      constexpr bool kC = decltype(compute_tag)::value;
+      tile_attend_pp<kExtWaves, kPages != kRowPages, kFp8, kC, kPages == kSetPages, kNt>(
+          a.kv, scale, bt_row, g, 0, t_end, t_full, limit, qv, lds, o, m_run, l_run, bad);
+    };
+    if (active)
+      attend(std::true_type{});
+    else
+      attend(std::false_type{});
+  }
 
   const float l_tot = sum_l32(l_run);
   if (row_ok) {
@@ -255,6 +267,15 @@ hipError_t launch_extend(const ExtendArgs& a, hipStream_t stream, KernelTimer* t
   const bool once = a.decode_rows > 0 && a.head_blocks == 1 && a.decode_rows <= a.tile_tokens;
   auto go = [&](auto fp8_tag) {
     constexpr bool kF = decltype(fp8_tag)::value;
+    if constexpr (!kF) {
+      if (pages == kStepPages && !a.staged) {
+        if (once)
+          extend_mfma_kernel<false, kDirectPages, true><<<grid, kExtWaves * 64, 0, stream>>>(a);
+        else
+          extend_mfma_kernel<false, kDirectPages><<<grid, kExtWaves * 64, 0, stream>>>(a);
+        return;
+      }
+    }
     if (pages == kStepPages && once)
       extend_mfma_kernel<kF, kStepPages, true><<<grid, kExtWaves * 64, 0, stream>>>(a);
     else if (pages == kStepPages)

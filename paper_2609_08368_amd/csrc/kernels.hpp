@@ -138,6 +138,12 @@ struct ExtendArgs {
   // not read), and the rows of empty sequences are written as zeros with
   // lse = -inf
   int decode_rows;
+  // nonzero: bf16 pages take the 64-key register-staged steps as FP8 pages do
+  // (a multi-token decode routed through extend units, which owes extend no
+  // bitwise agreement and streams its rows faster that way); zero: pages of
+  // at least 64 keys take 128-key steps, as every extend and deterministic
+  // decode does
+  int staged;
   // nullable: the extend planner queues no unit (and writes nothing) when
   // *gate != 0, i.e. when the decode planner that runs before it found shared
   // prefix pages and the split passes compute the rows

@@ -650,6 +650,7 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
       return fail(RL_ERR_UNSUPPORTED,
                   "deterministic multi-token decode needs q, out and lse_out with batch stride = tokens x token stride");
     rl::ExtendArgs x = extend_rows();
+    x.staged = o.deterministic ? 0 : 1;
     return run_extend(x, st, 0, noalloc);
   }
   int dev = 0;
@@ -734,6 +735,7 @@ int decode_impl(const rl_tensor* q, const rl_tensor* k_pages, const rl_tensor* v
   int rc = RL_OK;
   if (e == hipSuccess) {
     rl::ExtendArgs x = extend_rows();
+    x.staged = 1;
     x.gate = a.ws.hdr + 3;
     const WsView xw{base + ext_off, w.err};
     rc = run_extend(x, st, 0, noalloc, &xw, false);

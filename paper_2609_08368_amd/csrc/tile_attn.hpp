@@ -1,5 +1,6 @@
 // Multi-row attention tile on MFMA 32x32x16, shared by the extend kernel
-// (rows = chunk tokens x query heads; tile_attend_pp), the group-prefix kernel
+// (rows = chunk tokens x query heads; tile_attend_pp, and tile_attend_dl with
+// 128-key steps for bf16 pages of at least 64 keys), the group-prefix kernel
 // (rows = trajectory-group members x query heads) and the multi-token decode
 // kernel (rows = query tokens x query heads; both tile_attend). A workgroup of
 // kWaves waves owns up to 32 * kWaves query rows that all read the same keys
@@ -558,6 +559,332 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
   }
   mfma_phase(yes, no, (nsteps - 1) & 1, 0);
   if (!late) __syncthreads();
+}
+
+// ---- 128-key steps, rows loaded straight into LDS ---------------------------
+// The ping-pong schedule above with steps of 128 keys (one MFMA phase holds the
+// 32 S^T MFMAs of a step and the 32 PV MFMAs of the one before, so barriers and
+// phase switches per flop are halved) and bf16 rows moved from global memory
+// into LDS by the load itself (global_load_lds_dwordx4): no row passes through
+// registers and no wave writes LDS, which leaves room for the doubled score and
+// probability tiles.
+//
+// LDS layout of a step's K (and V): 32 blocks of four 256-byte rows, padded to
+// kDlKPitch (kDlVPitch) bytes. Row r of the step sits in block r % 16 + 16 (r / 64)
+// at slot (r / 16) % 4, so
+//  * one load instruction fills one block (lane l -> slot l / 16, 16-byte chunk
+//    l % 16), and a block's rows lie in one 64-key half of the step, i.e. in
+//    one page: the wave's address is a scalar page base plus a lane offset;
+//  * the K operand read (32 consecutive rows, one 16-byte chunk each) and the
+//    transposed V read are a per-lane base plus compile-time offsets;
+//  * 16 consecutive K rows fall in 16 blocks whose padding puts them on
+//    distinct 4-bank groups, and the four rows a 16-lane group of the
+//    transposed V read touches sit 16 banks apart (no bank conflicts).
+// Each of the two K and two V buffers is its own LDS array, and the step loop
+// is unrolled by two so every access names its array: the compiler then knows
+// that the operand reads of a phase do not touch the arrays the loads in
+// flight write, and waits for those loads only where their rows are read.
+constexpr int kDlKeys = 128;
+constexpr int kDlKPitch = 1024 + 16;
+constexpr int kDlVPitch = 1024 + 64;
+constexpr int kDlKBytes = 32 * kDlKPitch;
+constexpr int kDlVBytes = 32 * kDlVPitch;
+
+// Attention of this lane's query column over keys [0, t_hi) of KV head g, as
+// tile_attend_pp (same arguments and results) for bf16 pages of at least 64
+// keys whose in-page offsets fit 31 bits. Its rounding differs from the
+// 64-key routines (the running max and the sums advance per 128 keys).
+// Schedule: the rows of K(j+1) and V(j) are requested after the barrier that
+// ends the second group's MFMA phase of step j-1 (the last reads of the
+// buffers they fill): by the first group between the first eight MFMAs of its
+// phase j, by the second group at the start of its softmax phase j-1. Each
+// wave waits for its own loads before the barrier after which they are first
+// read, one MFMA phase and one softmax phase later.
+template <bool kCompute, bool kNt>
+__device__ __forceinline__ void tile_attend_dl(const PagedKV& kv, float scale, const int* bt_row, int g, int t_hi,
+                                               int t_full, int limit, const bf16x8 (&qv)[8], char* kl0, char* kl1,
+                                               char* vl0, char* vl1, f32x16 (&o)[4], float& m_run, float& l_run,
+                                               int& bad) {
+  constexpr int kAhead = 3;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int col = lane & 31, kg = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool late = wave >= 4;
+  const float sl2 = scale * kLog2e;
+  if (t_hi <= 0) return;
+  const int nsteps = (t_hi + kDlKeys - 1) / kDlKeys;
+  const int pmask = kv.page_size - 1;
+
+  // loads: wave w fills blocks w + 8 i (i = 0..3) of K and of V; block b holds
+  // rows b % 16 + 16 s (s = lane / 16) of half b / 16, chunk lane % 16
+  typedef __attribute__((address_space(4))) const int ConstInt;
+  const ConstInt* bt_c = (const ConstInt*)bt_row;
+  const char* kbase = (const char*)kv.k + 2 * ((int64_t)g * kv.sh);
+  const char* vbase = (const char*)kv.v + 2 * ((int64_t)g * kv.v_sh);
+  const uint32_t kss = (uint32_t)kv.ss, vss = (uint32_t)kv.v_ss;
+  const int lrow = wave + 16 * (lane >> 4);          // row in its half of block w (blocks w + 16 add 0)
+  const uint32_t lchunk = 16u * (uint32_t)(lane & 15);
+  // page ids of the two halves of step j (scalar loads; a half past the last
+  // key takes the first half's page)
+  auto page_pair = [&](int j, int (&p)[2]) {
+    const int t0 = j * kDlKeys;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int t = (t0 + 64 * h < t_hi) ? t0 + 64 * h : t0;
+      int pg = bt_c[__umul24((uint32_t)(t >> kv.log2_page), (uint32_t)kv.bt_sj)];
+      if ((unsigned)pg >= (unsigned)kv.num_pages) {
+        bad = 1;
+        pg = pg < 0 ? 0 : kv.num_pages - 1;
+      }
+      p[h] = pg;
+    }
+  };
+  // block w + 8 i of step j's rows into one buffer; rows past the last key
+  // load that key again
+  auto dma_block = [&](int j, const int (&p)[2], const char* base, int64_t sp, uint32_t ss, char* dst, int pitch,
+                       int i) {
+    const int t0 = j * kDlKeys;
+    {
+      const int h = i >> 1;
+      const int hh = (t0 + 64 * h < t_hi) ? h : 0;    // the half whose page this block reads
+      const int last = min(63, t_hi - 1 - t0 - 64 * hh);
+      const int row = min(lrow + 8 * (i & 1), last);
+      const char* sbase = base + 2 * ((int64_t)p[h] * sp + (int64_t)((t0 + 64 * hh) & pmask) * ss);
+      const uint32_t voff = 2u * (uint32_t)row * ss + lchunk;
+      const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)(dst + (wave + 8 * i) * pitch);
+      // Issued as assembly: the compiler would otherwise wait for every row
+      // load in flight before LDS reads it cannot tell apart from the loads'
+      // destinations (the transposed V reads), stalling the MFMA phase. The
+      // rows' readers are ordered by wait_loads and the barriers instead; a
+      // wait the compiler counts for its own loads can only be lengthened by
+      // these (loads complete in order).
+      if constexpr (kNt)
+        asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2 nt" ::"s"(lds), "v"(voff), "s"(sbase)
+                     : "memory", "m0");
+      else
+        asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(sbase)
+                     : "memory", "m0");
+    }
+  };
+  auto dma = [&](int j, const int (&p)[2], const char* base, int64_t sp, uint32_t ss, char* dst, int pitch) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma_block(j, p, base, sp, ss, dst, pitch, i);
+  };
+  auto wait_loads = [&]() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
+  // A workgroup barrier without the memory fence of __syncthreads: the row
+  // loads are ordered explicitly instead. A wave waits for its own row loads
+  // (wait_loads) before the barrier after which they are read, and every LDS
+  // operand read of a phase is consumed by that phase's MFMAs before the
+  // barrier that ends it. The empty asm statements keep the compiler from
+  // moving LDS accesses across the barrier.
+  auto barrier = [&]() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+
+  // operand reads: per-lane bases (see the layout above)
+  const int kread = (col & 15) * kDlKPitch + (col >> 4) * 256 + 16 * kg;
+  const int tr_row = 4 * kg + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const int vread = tr_row * kDlVPitch + 2 * tr_col;
+
+  f32x16 sc[4];
+  bf16x8 pb[8];
+
+  // hook(ii) runs after the ii-th MFMA of the phase, ii < 8 (the first
+  // group's row loads, spread between MFMAs so their address arithmetic
+  // issues while the MFMAs run)
+  auto mfma_phase = [&](auto pv_tag, auto s_tag, const char* vbuf, const char* kbuf, auto&& hook) {
+    if constexpr (!kCompute) {
+#pragma unroll
+      for (int ii = 0; ii < 8; ++ii) hook(ii);
+      return;
+    }
+    constexpr bool kPV = decltype(pv_tag)::value, kS = decltype(s_tag)::value;
+    constexpr int i0 = kPV ? 0 : 32, i1 = kS ? 64 : 32;
+    const f32x16 zero = {};
+    auto read = [&](int i) -> bf16x8 {
+      if (i < 32) {
+        const int h = i >> 2, jd = i & 3;
+        const char* vp = vbuf + vread + 16 * (h >> 2) * kDlVPitch + 256 * (h & 3) + 64 * jd;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)vp);
+        const i16x4 up = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vp + 8 * kDlVPitch));
+        return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+      const int c = (i - 32) >> 2, kb = (i - 32) & 3;
+      return *reinterpret_cast<const bf16x8*>(kbuf + kread + 16 * (kb >> 1) * kDlKPitch + 512 * (kb & 1) + 32 * c);
+    };
+    // the PV MFMAs of the previous step go first: P^T is dead before the
+    // scores of this step are born (the first MFMA of each score chain takes a
+    // zero accumulator), which keeps the phase within the register file
+    bf16x8 ring[kAhead + 1];
+    auto at = [&](int ii) { return i0 + ii; };
+    constexpr int n = i1 - i0;
+#pragma unroll
+    for (int ii = 0; ii < kAhead; ++ii) ring[ii % (kAhead + 1)] = read(at(ii));
+#pragma unroll
+    for (int ii = 0; ii < n; ++ii) {
+      const int i = at(ii);
+      if (ii + kAhead < n) ring[(ii + kAhead) % (kAhead + 1)] = read(at(ii + kAhead));
+      __builtin_amdgcn_sched_barrier(0);
+      if (i < 32)
+        o[i & 3] = mfma_32x32x16(ring[ii % (kAhead + 1)], pb[i >> 2], o[i & 3]);
+      else
+        sc[(i - 32) & 3] =
+            mfma_32x32x16(ring[ii % (kAhead + 1)], qv[(i - 32) >> 2], i < 36 ? zero : sc[(i - 32) & 3]);
+      __builtin_amdgcn_sched_barrier(0);
+      if (ii < 8) {
+        hook(ii);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  };
+
+  auto softmax_phase = [&](int t0) {
+    if constexpr (!kCompute) return;
+    float mt = kNegInf;
+    if (t0 + kDlKeys > t_full) {
+      // a key is visible when it is at most this lane's last visible key; the
+      // fences keep each compare next to its select (hoisted, the 64 compare
+      // masks would not fit the scalar registers)
+      const int d = min(limit, t_hi - 1) - t0 - 4 * kg;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          if (32 * kb + 8 * (e >> 2) + (e & 3) > d) sc[kb][e] = kNegInf;
+          if ((e & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; e += 2) mt = fmaxf(mt, fmaxf(sc[kb][e], sc[kb][e + 1]));
+    mt = max_l32(mt) * sl2;
+    const bool raise = mt > m_run + kLazy;
+    if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+      const float m_new = raise ? mt : m_run;
+      const float alpha = exp2_fast(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int jd = 0; jd < 4; ++jd) o[jd] *= alpha;
+      m_run = m_new;
+    }
+    const float neg_m = -m_run;
+    float ps[4] = {0.f, 0.f, 0.f, 0.f};
+    // one 16-key group at a time (fenced), so the scores die as their
+    // probabilities are packed
+#pragma unroll
+    for (int h = 0; h < 8; ++h) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float p = exp2_fast(fmaf(sc[h >> 1][8 * (h & 1) + e], sl2, neg_m));
+        ps[e & 3] += p;
+        pb[h][e] = (__bf16)p;
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
+    // P^T and the row sum are formed here, in the softmax phase: without
+    // these pins the compiler sinks the exponentials (or the sum's additions)
+    // past the barrier into the next MFMA phase, where their 64 fp32 values
+    // would sit beside the new scores
+#pragma unroll
+    for (int h = 0; h < 8; ++h) asm volatile("" : "+v"(pb[h]));
+    asm volatile("" : "+v"(l_run));
+  };
+
+  const std::true_type yes{};
+  const std::false_type no{};
+  // page ids of steps j (pv, for V) and j+1 (pk, for K) at each issue; the ids
+  // of the step after are read at the end of a softmax phase, where the
+  // barrier's wait covers the scalar load (an outstanding scalar load would
+  // make the MFMA phase's LDS reads wait for it too)
+  int pv[2], pk[2];
+  int pid_next = 2;                                  // step whose ids the next read fetches
+  page_pair(0, pv);
+  dma(0, pv, kbase, kv.sp, kss, kl0, kDlKPitch);
+  if (nsteps > 1) page_pair(1, pk);
+  wait_loads();
+  barrier();
+  auto next_pages = [&]() {
+    if (pid_next < nsteps) page_pair(pid_next, pk);
+  };
+  // the two groups run the same steps with their loads, waits and barriers
+  // placed as described above; kLate is the second group
+  auto run = [&](auto late_tag) {
+    constexpr bool kLate = decltype(late_tag)::value;
+    // loads of K(j+1) and V(j), block by block (ii = 0..7); buffers by the
+    // parity of j
+    auto issue_block = [&](int j, auto par, int ii) {
+      constexpr int P = decltype(par)::value;
+      if (ii < 4) {
+        if (j + 1 < nsteps) dma_block(j + 1, pk, kbase, kv.sp, kss, P ? kl0 : kl1, kDlKPitch, ii);
+      } else {
+        dma_block(j, pv, vbase, kv.v_sp, vss, P ? vl1 : vl0, kDlVPitch, ii - 4);
+      }
+    };
+    auto issue_done = [&](int j) {
+      pv[0] = pk[0];
+      pv[1] = pk[1];
+      pid_next = j + 2;
+    };
+    auto issue = [&](int j, auto par) {
+#pragma unroll
+      for (int ii = 0; ii < 8; ++ii) issue_block(j, par, ii);
+      issue_done(j);
+    };
+    const auto none = [](int) {};
+    if constexpr (kLate) {
+      issue(0, std::integral_constant<int, 0>{});
+      next_pages();
+      barrier();
+    }
+    // step j: K(j) in buffer j % 2, V(j-1) in buffer (j-1) % 2
+    auto body = [&](int j, auto par, auto first) {
+      constexpr int P = decltype(par)::value;
+      char* kcur = P ? kl1 : kl0;
+      char* vprev = P ? vl0 : vl1;
+      auto hook = [&](int ii) {
+        if constexpr (!kLate) issue_block(j, par, ii);
+      };
+      if constexpr (decltype(first)::value)
+        mfma_phase(no, yes, vprev, kcur, hook);
+      else
+        mfma_phase(yes, yes, vprev, kcur, hook);
+      if constexpr (!kLate) issue_done(j);
+      if constexpr (kLate) wait_loads();
+      barrier();
+      if constexpr (kLate) {
+        if (j + 1 < nsteps) issue(j + 1, std::integral_constant<int, 1 - P>{});
+      }
+      softmax_phase(j * kDlKeys);
+      next_pages();
+      if constexpr (!kLate) wait_loads();
+      barrier();
+    };
+    const std::integral_constant<int, 0> even{};
+    const std::integral_constant<int, 1> odd{};
+    body(0, even, yes);
+    int j = 1;
+    for (; j + 1 < nsteps; j += 2) {
+      body(j, odd, no);
+      body(j + 1, even, no);
+    }
+    if (j < nsteps) body(j, odd, no);
+    // PV of the final step: V(n-1) in buffer (n-1) % 2
+    if ((nsteps - 1) & 1)
+      mfma_phase(yes, no, vl1, kl0, none);
+    else
+      mfma_phase(yes, no, vl0, kl0, none);
+    if constexpr (!kLate) barrier();
+  };
+  if (late)
+    run(std::true_type{});
+  else
+    run(std::false_type{});
 }
 
 // Normalised output row of this lane's column: element (jd, q, i) of o holds

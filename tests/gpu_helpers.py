@@ -72,6 +72,22 @@ def run_decode(w: wl.Paged, tensors: dict, out_dtype=torch.bfloat16, **opts):
     return out, lse
 
 
+def pages_below(tensors: dict, size: int) -> dict:
+    """The same keys in pages of fewer than `size` keys: each halving turns page i
+    into pages 2i and 2i + 1 (K, V and the block table; nothing else changes). bf16
+    pages of fewer than 64 keys take the 64-key steps, so this gives the reference
+    for paths that advance 64 keys per step whatever the page size."""
+    t = dict(tensors)
+    while t["k_pages"].shape[1] >= size:
+        for name in ("k_pages", "v_pages"):
+            n, p = t[name].shape[:2]
+            t[name] = t[name].reshape(2 * n, p // 2, *t[name].shape[2:])
+        bt = t["block_table"]
+        two = torch.stack((2 * bt, 2 * bt + 1), dim=-1).reshape(bt.shape[0], -1)
+        t["block_table"] = torch.where(two >= 0, two, torch.full_like(two, -1)).contiguous()
+    return t
+
+
 def run_extend(w: wl.Paged, tensors: dict, out_dtype=torch.bfloat16, **opts):
     q = tensors["q"]
     out = poison_like(torch.empty(q.shape, dtype=out_dtype, device=q.device))

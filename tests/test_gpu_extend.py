@@ -21,6 +21,12 @@ CASES = [
     (16, 24, 2, [80, 33], [17, 33]),                 # GQA 12: 10 tokens per tile
     (16, 256, 1, [40, 9], [3, 2]),                   # GQA 256: two 128-head blocks
     (128, 8, 1, [600], [257]),
+    # 128-key steps (bf16 pages of at least 64 keys): one step, a step whose second
+    # 64-key half lies past the last key, exact multiples of 128, both halves of a step
+    # in one page (the second starting inside it), a short second sequence
+    (64, 16, 2, [1, 64, 65, 128, 129, 192, 193, 256], [1, 64, 1, 128, 3, 64, 100, 256]),
+    (128, 8, 2, [1000, 255, 256, 257], [300, 255, 1, 257]),
+    (128, 32, 4, [130, 380], [130, 60]),
     (16, 8, 2, [30, 0, 12], [0, 0, 12]),             # empty chunks
 ]
 

@@ -114,11 +114,12 @@ def test_mtp_deterministic_equals_extend(n):
 @pytest.mark.parametrize("n", [2, 8])
 def test_mtp_unshared_runs_as_deterministic(n):
     """With prefix sharing off and automatic splits, multi-token decode runs through
-    the extend kernel: bitwise the deterministic mode, and the oracle's values."""
+    the extend kernel's 64-key steps: bitwise the deterministic mode over the same keys
+    in pages of 32 (which take those steps too), and the oracle's values."""
     w, t = mtp_problem(185 + n, [n, 333, 1500, 64 + n], n, 96, 8, 64)
     H.say(f"mtp unshared n={n}")
     out, lse = run_mtp(w, t, n, prefix_share=False)
-    do, dl = run_mtp(w, t, n, deterministic=True)
+    do, dl = run_mtp(w, H.pages_below(t, 64), n, deterministic=True)
     assert torch.equal(out.view(torch.int16), do.view(torch.int16)) and torch.equal(lse, dl)
     check(w, t, n, out, lse, f"mtp unshared n={n}")
     ra.check_device_errors()
@@ -149,12 +150,13 @@ def test_mtp_unshared_split_path_cases():
 @pytest.mark.parametrize("n", [2, 8])
 def test_mtp_route_follows_shared_pages(n):
     """Prefix sharing on, bf16 pages, automatic splits: a batch without shared pages is
-    computed by the queued extend pass (bitwise the deterministic mode); a trajectory-group
-    batch by the split passes, whose rows the extend pass must leave alone."""
+    computed by the queued extend pass (bitwise the deterministic mode over the same keys
+    in pages of 32: both advance 64 keys per step); a trajectory-group batch by the split
+    passes, whose rows the extend pass must leave alone."""
     w, t = mtp_problem(190 + n, [n, 300, 1400, 64 + n], n, 96, 8, 64)
     H.say(f"mtp route without shared pages n={n}")
     out, lse = run_mtp(w, t, n)
-    do, dl = run_mtp(w, t, n, deterministic=True)
+    do, dl = run_mtp(w, H.pages_below(t, 64), n, deterministic=True)
     assert torch.equal(out.view(torch.int16), do.view(torch.int16)) and torch.equal(lse, dl)
     check(w, t, n, out, lse, f"mtp route no sharing n={n}")
     gs, shared = 4, 1024
