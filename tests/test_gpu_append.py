@@ -74,6 +74,28 @@ def test_append_matches_oracle_bitwise(case, fp8):
     ra.check_device_errors()
 
 
+@pytest.mark.parametrize("fp8", [False, True])
+@pytest.mark.parametrize("batch", [64, 128, 255, 256, 300])
+def test_append_many_sequences(batch, fp8):
+    """Batches past the FP8 owner search's wave-wide form (up to 63 sequences; a binary
+    search from 64 on, as for bf16 pages): decode-like steps of zero to two rows per
+    sequence, empty ones mixed in, 8 KV heads."""
+    rng = np.random.default_rng(160 + batch)
+    ql = rng.choice([0, 1, 1, 1, 2], size=batch)
+    ql[0], ql[-1] = 0, 1                       # an empty first chunk, a row in the last
+    kv = ql + rng.integers(0, 70, size=batch)
+    w = wl.custom(160 + batch, "extend", [int(x) for x in kv], q_lens=[int(x) for x in ql], hq=8, hkv=8,
+                  page_size=16)
+    H.say(f"append {batch} sequences fp8={fp8}")
+    t = (wl.materialize_fp8 if fp8 else wl.materialize)(w, DEV)
+    k, v = new_rows(w, 9 + batch)
+    kp, vp = run_append(t, k, v, fp8)
+    ok, ov = oracle_append(w, t, k, v, fp8)
+    assert np.array_equal(host(kp), ok), "K pool differs from the oracle's"
+    assert np.array_equal(host(vp), ov), "V pool differs from the oracle's"
+    ra.check_device_errors()
+
+
 def test_append_fp8_rounding_and_saturation():
     """Near-ties where the float32 quotient decides the code, values beyond 448 x scale
     (saturate), zeros of both signs, and values in the subnormal range."""
