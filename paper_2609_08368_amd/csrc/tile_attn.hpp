@@ -578,12 +578,11 @@ __device__ __forceinline__ void tile_attend_pp(const PagedKV& kv, float scale, c
 //  * the K operand read (32 consecutive rows, one 16-byte chunk each) and the
 //    transposed V read are a per-lane base plus compile-time offsets;
 //  * 16 consecutive K rows fall in 16 blocks whose padding puts them on
-//    distinct 4-bank groups, and the four rows a 16-lane group of the
+//    distinct 4-bank groups, and the four rows each 32-lane group of the
 //    transposed V read touches sit 16 banks apart (no bank conflicts).
 // Each of the two K and two V buffers is its own LDS array, and the step loop
-// is unrolled by two so every access names its array: the compiler then knows
-// that the operand reads of a phase do not touch the arrays the loads in
-// flight write, and waits for those loads only where their rows are read.
+// is unrolled by two, so every operand read names its buffer and adds a
+// compile-time offset.
 constexpr int kDlKeys = 128;
 constexpr int kDlKPitch = 1024 + 16;
 constexpr int kDlVPitch = 1024 + 64;
@@ -623,7 +622,9 @@ __device__ __forceinline__ void tile_attend_dl(const PagedKV& kv, float scale, c
   const char* kbase = (const char*)kv.k + 2 * ((int64_t)g * kv.sh);
   const char* vbase = (const char*)kv.v + 2 * ((int64_t)g * kv.v_sh);
   const uint32_t kss = (uint32_t)kv.ss, vss = (uint32_t)kv.v_ss;
-  const int lrow = wave + 16 * (lane >> 4);          // row in its half of block w (blocks w + 16 add 0)
+  // row of this lane's slot within its half of the step, for blocks w and
+  // w + 16 (blocks w + 8 and w + 24 hold the rows 8 further)
+  const int lrow = wave + 16 * (lane >> 4);
   const uint32_t lchunk = 16u * (uint32_t)(lane & 15);
   // page ids of the two halves of step j (scalar loads; a half past the last
   // key takes the first half's page)
@@ -645,27 +646,24 @@ __device__ __forceinline__ void tile_attend_dl(const PagedKV& kv, float scale, c
   auto dma_block = [&](int j, const int (&p)[2], const char* base, int64_t sp, uint32_t ss, char* dst, int pitch,
                        int i) {
     const int t0 = j * kDlKeys;
-    {
-      const int h = i >> 1;
-      const int hh = (t0 + 64 * h < t_hi) ? h : 0;    // the half whose page this block reads
-      const int last = min(63, t_hi - 1 - t0 - 64 * hh);
-      const int row = min(lrow + 8 * (i & 1), last);
-      const char* sbase = base + 2 * ((int64_t)p[h] * sp + (int64_t)((t0 + 64 * hh) & pmask) * ss);
-      const uint32_t voff = 2u * (uint32_t)row * ss + lchunk;
-      const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)(dst + (wave + 8 * i) * pitch);
-      // Issued as assembly: the compiler would otherwise wait for every row
-      // load in flight before LDS reads it cannot tell apart from the loads'
-      // destinations (the transposed V reads), stalling the MFMA phase. The
-      // rows' readers are ordered by wait_loads and the barriers instead; a
-      // wait the compiler counts for its own loads can only be lengthened by
-      // these (loads complete in order).
-      if constexpr (kNt)
-        asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2 nt" ::"s"(lds), "v"(voff), "s"(sbase)
-                     : "memory", "m0");
-      else
-        asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(sbase)
-                     : "memory", "m0");
-    }
+    const int h = i >> 1;
+    const int hh = (t0 + 64 * h < t_hi) ? h : 0;      // the half whose page this block reads
+    const int last = min(63, t_hi - 1 - t0 - 64 * hh);
+    const int row = min(lrow + 8 * (i & 1), last);
+    const char* sbase = base + 2 * ((int64_t)p[h] * sp + (int64_t)((t0 + 64 * hh) & pmask) * ss);
+    const uint32_t voff = 2u * (uint32_t)row * ss + lchunk;
+    const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)(dst + (wave + 8 * i) * pitch);
+    // Issued as assembly: the compiler would otherwise wait for every row load
+    // in flight before LDS reads it cannot tell apart from the loads'
+    // destinations (the transposed V reads), stalling the MFMA phase. The
+    // rows' readers are ordered by wait_loads and the barriers instead; a wait
+    // the compiler counts for its own loads can only be lengthened by these
+    // (loads complete in order).
+    // (m0 holds the LDS address: an input operand, so the compiler sets it)
+    if constexpr (kNt)
+      asm volatile("global_load_lds_dwordx4 %0, %1 nt" ::"v"(voff), "s"(sbase), "{m0}"(lds) : "memory");
+    else
+      asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "{m0}"(lds) : "memory");
   };
   auto dma = [&](int j, const int (&p)[2], const char* base, int64_t sp, uint32_t ss, char* dst, int pitch) {
 #pragma unroll
